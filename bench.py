@@ -1,0 +1,216 @@
+#!/usr/bin/env python3
+"""Throughput of the candidate-scoring step on one MI355X.
+
+One step = validity filter (model V) -> performance prediction over the
+accepted candidates (model P) -> top-k selection, over a pool that is
+already resident in HBM, through the C ABI (libml2.so).  The default
+workload is the 16M-candidate pool (16,777,216 x 128 features; V: 300 trees
+of depth 6; P: 1000 trees of depth 8; k = 1024).
+
+Prints ONE JSON line.  `value` is candidates scored+filtered per second.
+The `roofline` object covers the dominant kernel (the performance walk),
+with achieved node visits/s measured with HIP events on the launch stream.
+The `cpu_baseline` object times the CPU oracle (all host cores) on a
+bounded sample of the same pool.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME]
+    python bench.py --copy-probe      # plain 1 GiB device copies (counter scale)
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+# VALU lane-issue ceiling of the chip: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz
+VALU_LANE_OPS_PER_S = 256 * 4 * 16 * 2.4e9
+METRIC = "candidate configs scored+filtered/sec (validity+perf+top-k); % of HBM peak"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "perf_walk_roofline_traffic.json")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2411_10764_amd", "csrc", "walk_kernels.hip")
+
+
+def _log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def _kernel_sha() -> str:
+    with open(KERNEL_SOURCE, "rb") as fh:
+        return hashlib.sha256(fh.read()).hexdigest()
+
+
+def _traffic(kernel_sha: str):
+    """HBM bytes per launch of the perf walk from committed rocprofv3 counter
+    runs, or None when absent or taken on a different kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            t = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_source_sha256") != kernel_sha:
+        return None
+    return t.get("bytes_per_launch")
+
+
+def copy_probe() -> None:
+    import torch
+    n = 1 << 28  # 1 GiB of float32
+    a = torch.ones(n, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(5):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": 4 * n, "launches": 5}))
+
+
+def cpu_baseline(w, rows: int):
+    import gen
+    import oracle
+    threads = gen.default_threads()
+    X = w.features(rows=np.arange(rows, dtype=np.int64))
+    V, P = oracle.OracleEnsemble(w.validity()), oracle.OracleEnsemble(w.perf())
+    t0 = time.perf_counter()
+    oracle.pipeline(V, P, X, w.k, threads=threads)
+    dt = time.perf_counter() - t0
+    return {"value": rows / dt, "unit": "candidates/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {rows} candidates of the {w.name} pool ({w.F} features), "
+                      f"validity -> masked perf -> top-{w.k}, {dt:.2f} s wall on {threads} "
+                      f"threads ({os.cpu_count()} visible cpus)"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="roofline")
+    ap.add_argument("--cpu-rows", type=int, default=1 << 20)
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true")
+    args = ap.parse_args()
+
+    if args.copy_probe:
+        copy_probe()
+        return 0
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
+              "(the pool would shard by rows with one all-gather of the per-GPU top-k lists).",
+              file=sys.stderr)
+        return 2
+
+    import torch
+    import gen
+    from paper_2411_10764_amd import ml2
+
+    w = gen.WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    _log(f"workload {w.name}: n={w.n} F={w.F} V={w.v_trees}x{w.v_depth} "
+         f"P={w.p_trees}x{w.p_depth} k={w.k}; generating features")
+    t0 = time.perf_counter()
+    X = torch.empty((w.n, w.F), dtype=torch.float32, device=dev)
+    chunk = 1 << 21
+    host = np.empty((chunk, w.F), np.float32)
+    for r0 in range(0, w.n, chunk):
+        m = min(chunk, w.n - r0)
+        gen.features(w.seed, m, w.F, w.K, row0=r0, out=host[:m])
+        X[r0:r0 + m].copy_(torch.from_numpy(host[:m]))
+    torch.cuda.synchronize()
+    del host
+    _log(f"features resident in HBM ({X.numel() * 4 / 2**30:.2f} GiB) in "
+         f"{time.perf_counter() - t0:.1f} s")
+
+    v = ml2.ml2_load_ensemble(w.validity())
+    p = ml2.ml2_load_ensemble(w.perf())
+    pipe = ml2.Pipeline(v, p, w.n, w.k, device=dev)
+    stream = torch.cuda.current_stream()
+
+    for _ in range(args.warmup):
+        pipe.run(X)
+    torch.cuda.synchronize()
+    _log(f"warmup done ({args.warmup} steps)")
+
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    start = time.perf_counter()
+    for s in range(args.steps):
+        e = ev[s]
+        e[0].record(stream)
+        ml2.ml2_score_validity(v, X, pipe.valid, None, stream)
+        e[1].record(stream)
+        ml2.ml2_score_perf(p, X, pipe.valid, pipe.score, stream)
+        e[2].record(stream)
+        ml2.ml2_filter_topk(pipe.valid, pipe.score, w.k, pipe.idx, pipe.top, pipe.num, pipe.ws,
+                            pipe.ws_bytes, w.n, stream)
+        e[3].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - start
+    t_val = np.mean([e[0].elapsed_time(e[1]) for e in ev])
+    t_perf = np.mean([e[1].elapsed_time(e[2]) for e in ev])
+    t_topk = np.mean([e[2].elapsed_time(e[3]) for e in ev])
+    t_step = np.mean([e[0].elapsed_time(e[3]) for e in ev])
+    ms_per_step = 1000.0 * wall / args.steps
+    valid = pipe.valid.cpu().numpy()
+    n_valid = int(valid.sum())
+    num = int(pipe.num.item())
+    _log(f"step {ms_per_step:.3f} ms (events {t_step:.3f}): validity {t_val:.3f} ms, "
+         f"perf {t_perf:.3f} ms, top-k {t_topk:.3f} ms; valid {n_valid}/{w.n}, selected {num}")
+
+    value = w.n / (ms_per_step / 1000.0)
+    alg_bytes = 4.0 * w.F * w.n + w.n + 8.0 * w.k
+    visits_v = w.n * w.v_trees * w.v_depth
+    visits_p = n_valid * w.p_trees * w.p_depth
+    sha = _kernel_sha()
+    perf_visits_per_s = visits_p / (t_perf / 1000.0)
+    roofline = {
+        "bound": "alu",
+        "kernel": "perf_kernel (model P walk over accepted candidates)",
+        "achieved": perf_visits_per_s / 1e12,
+        "peak": VALU_LANE_OPS_PER_S / 1e12,
+        "unit": "Tvisit/s",
+        "frac": perf_visits_per_s / VALU_LANE_OPS_PER_S,
+        "traffic": _traffic(sha),
+        "work_per_launch": f"{visits_p} node visits ({n_valid} accepted x {w.p_trees} trees "
+                           f"x depth {w.p_depth})",
+        "launch_ms": t_perf,
+        "validity_kernel": {"achieved": visits_v / (t_val / 1000.0) / 1e12, "launch_ms": t_val,
+                            "frac": visits_v / (t_val / 1000.0) / VALU_LANE_OPS_PER_S},
+        "hbm": {"algorithmic_bytes_per_step": alg_bytes,
+                "achieved_gbs": alg_bytes / (ms_per_step / 1000.0) / 1e9,
+                "peak_gbs": HBM_PEAK_GBS,
+                "frac": alg_bytes / (ms_per_step / 1000.0) / 1e9 / HBM_PEAK_GBS},
+    }
+    out = {
+        "metric": METRIC, "value": value, "unit": "candidates/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded knob + lognormal features, random perfect trees)",
+        "config": {"workload": w.name, "candidates": w.n, "features": w.F,
+                   "knob_features": w.K, "validity": f"{w.v_trees} trees x depth {w.v_depth}",
+                   "perf": f"{w.p_trees} trees x depth {w.p_depth}", "k": w.k,
+                   "seed": w.seed, "invalid_fraction": 1 - n_valid / w.n},
+        "roofline": roofline,
+        "hbm_frac": roofline["hbm"]["frac"],
+        "kernel_ms": {"validity": t_val, "perf": t_perf, "topk": t_topk},
+    }
+    del X
+    torch.cuda.empty_cache()
+    if not args.no_cpu:
+        _log(f"cpu baseline: oracle on {args.cpu_rows} candidates")
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_rows)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

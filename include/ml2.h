@@ -1,0 +1,169 @@
+/*
+ * ml2.h -- C ABI of the candidate-scoring library (gfx950).
+ *
+ * The library implements the data-parallel step of ML2Tuner's configuration
+ * explorer (Section 2 and Fig. 1): every candidate configuration of a pool is
+ * scored by a validity model V and, where V accepts it, by a performance
+ * model P; the explorer then keeps the top (alpha+1)*N candidates by
+ * predicted performance among those V accepts ("ML Model V"; "Hidden Feature
+ * Extractor & ML Model A").  Both models are XGBoost gbtree ensembles
+ * (Section 3 "Experimental Setup"; Table 3: V uses the binary hinge
+ * objective, P the squared-error regression objective).
+ *
+ * Conventions shared by every call:
+ *   - A split sends a candidate LEFT iff x[feature] < threshold (XGBoost's
+ *     rule): a tie or a NaN feature goes right.
+ *   - A margin is base_score + leaf(tree 0) + leaf(tree 1) + ... computed in
+ *     float32 as a left fold in tree-index order, round-to-nearest-even, no
+ *     fused operations, subnormals kept.  Results are bit-identical to that
+ *     definition, whatever the launch shape.
+ *   - Candidate pools are row-major float32 matrices X[n][ld] in DEVICE
+ *     memory; row i is candidate i; only columns 0..num_features-1 are read.
+ *   - Every pointer argument except desc/out/bytes is a DEVICE pointer owned
+ *     by the caller; the library never frees caller memory.
+ *   - stream is a hipStream_t passed as void* (NULL = the null stream).  Work
+ *     is enqueued asynchronously on it; arguments are validated
+ *     synchronously before anything is enqueued, and a call that returns an
+ *     error has enqueued nothing.  Faults inside kernels surface at the
+ *     caller's next synchronisation of the stream.
+ *   - The device is the HIP device current on the calling thread.
+ *   - Errors are returned as status codes; ml2_last_error() gives a
+ *     thread-local description of the last non-OK status.
+ */
+#ifndef ML2_H
+#define ML2_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  ML2_OK = 0,
+  ML2_ERR_INVALID_ARG = 1,   /* malformed descriptor, bad pointer/size/stride */
+  ML2_ERR_UNSUPPORTED = 2,   /* valid input beyond this library's limits */
+  ML2_ERR_OUT_OF_MEMORY = 3, /* device or host allocation failed */
+  ML2_ERR_HIP = 4            /* a HIP runtime call or kernel launch failed */
+} ml2_status;
+
+/* Library limits (checked at load / call time, ML2_ERR_UNSUPPORTED beyond). */
+#define ML2_MAX_DEPTH 12        /* longest root-to-leaf path, in splits */
+#define ML2_MAX_FEATURES 256    /* num_features of an ensemble */
+#define ML2_MAX_TOPK 16384      /* k of ml2_filter_topk */
+
+typedef struct ml2_ensemble ml2_ensemble; /* opaque; immutable after load */
+
+/*
+ * A tree ensemble in XGBoost's general form (host arrays, read during
+ * ml2_load_ensemble only).
+ *   num_trees       T >= 1
+ *   num_features    F in [1, ML2_MAX_FEATURES]; split features lie in [0, F)
+ *   base_score      margin bias, the first term of the fold (finite)
+ *   tree_node_offset[T+1]  tree t owns global nodes off[t] .. off[t+1]-1;
+ *                   off[0] = 0, strictly increasing; node ids inside a tree
+ *                   are tree-local (0 = root)
+ *   left_child, right_child  tree-local child ids; -1 on BOTH marks a leaf;
+ *                   an internal node has both children in range
+ *   split_feature, split_threshold  internal nodes only (threshold not NaN;
+ *                   +-inf allowed)
+ *   leaf_value      leaves only; finite
+ * Every node of a tree must be reachable from its root exactly once (no
+ * cycles, no shared or orphan nodes), and no root-to-leaf path may have more
+ * than ML2_MAX_DEPTH splits.  The sum T * max|leaf| + |base_score| must stay
+ * below FLT_MAX / 2 so that no partial sum overflows.
+ */
+typedef struct {
+  int32_t num_trees;
+  int32_t num_features;
+  float base_score;
+  const int64_t *tree_node_offset;
+  const int32_t *left_child;
+  const int32_t *right_child;
+  const int32_t *split_feature;
+  const float *split_threshold;
+  const float *leaf_value;
+} ml2_ensemble_desc;
+
+/*
+ * Validate desc and build the device form of the ensemble on the current
+ * device (synchronous).  Models V, P and A of Section 2 are each loaded this
+ * way.  On success *out owns its device tables until ml2_free_ensemble; a
+ * loaded ensemble may be used from several threads and streams at once.
+ * Errors: INVALID_ARG (NULL pointers, malformed trees, out-of-range feature,
+ * NaN threshold, non-finite leaf, overflow bound), UNSUPPORTED (depth or F
+ * beyond the limits), OUT_OF_MEMORY, HIP.  *out is set to NULL on error.
+ */
+ml2_status ml2_load_ensemble(const ml2_ensemble_desc *desc, ml2_ensemble **out);
+
+/* Release an ensemble (NULL is ignored).  Synchronises the device first, so
+ * no work that uses it may still be pending. */
+void ml2_free_ensemble(ml2_ensemble *e);
+
+/* Number of features / trees / padded depth of a loaded ensemble (-1 on NULL). */
+int32_t ml2_ensemble_num_features(const ml2_ensemble *e);
+int32_t ml2_ensemble_num_trees(const ml2_ensemble *e);
+int32_t ml2_ensemble_depth(const ml2_ensemble *e);
+
+/*
+ * Validity filter (model V, Section 2 "ML Model V"; hinge decision of
+ * Table 3): for i in [0, n)
+ *   margin_i     = fold of v over row i of X
+ *   valid_out[i] = (margin_i > 0) ? 1 : 0          (uint8)
+ *   margin_out[i]= margin_i                        (if margin_out != NULL)
+ * X: float32 [n][ld] device, ld >= num_features(v), 4-byte aligned.
+ * valid_out: uint8 [n] device.  margin_out: float32 [n] device or NULL.
+ * n = 0 enqueues nothing.  Errors: INVALID_ARG (NULL ensemble/pointers with
+ * n > 0, n < 0 or n > INT32_MAX, ld < F, misaligned X), HIP.
+ */
+ml2_status ml2_score_validity(const ml2_ensemble *v, const float *X, int64_t n, int64_t ld,
+                              uint8_t *valid_out, float *margin_out, void *stream);
+
+/*
+ * Performance prediction over the candidates V accepted (model P, Section 2
+ * "ML Model P"; regression objective of Table 3): for i in [0, n)
+ *   score_out[i] = fold of p over row i of X   if valid == NULL or valid[i] != 0
+ *                = -infinity                   otherwise
+ * Only accepted rows are read from X and walked.
+ * X as in ml2_score_validity; valid: uint8 [n] device or NULL (all accepted);
+ * score_out: float32 [n] device.  Errors as ml2_score_validity.
+ */
+ml2_status ml2_score_perf(const ml2_ensemble *p, const float *X, int64_t n, int64_t ld,
+                          const uint8_t *valid, float *score_out, void *stream);
+
+/* Device workspace bytes ml2_filter_topk needs for (n, k).  Errors:
+ * INVALID_ARG (NULL bytes, n < 0, k < 0), UNSUPPORTED (k > ML2_MAX_TOPK). */
+ml2_status ml2_topk_workspace_bytes(int64_t n, int32_t k, size_t *bytes);
+
+/*
+ * Selection of the configurations to pass on (Section 2: the explorer keeps
+ * the highest predicted performance among the candidates V accepts, until
+ * (alpha+1)*N are held; here k = (alpha+1)*N on a fixed pool).
+ * A candidate is included iff (valid == NULL or valid[i] != 0) and
+ * scores[i] is not NaN.  The included candidates are ordered by score
+ * descending, then index ascending (-0.0 and +0.0 are equal, so ties between
+ * them go to the lower index).  Writes
+ *   topk_idx[j], topk_score[j]  for j < min(k, #included): index and its
+ *                               score value (bit-exact copy of scores[idx])
+ *   topk_idx[j] = -1, topk_score[j] = -inf for the remaining slots
+ *   *num_selected = min(k, #included)          (int32, device)
+ * valid: uint8 [n] device or NULL; scores: float32 [n] device;
+ * topk_idx: int32 [k], topk_score: float32 [k], num_selected: int32 [1],
+ * workspace: >= ml2_topk_workspace_bytes(n, k) bytes of device memory,
+ * 256-byte aligned, used exclusively by this call until it completes.
+ * Errors: INVALID_ARG (NULL pointers, n/k out of range, small workspace),
+ * UNSUPPORTED (k > ML2_MAX_TOPK), HIP.
+ */
+ml2_status ml2_filter_topk(const uint8_t *valid, const float *scores, int64_t n, int32_t k,
+                           int32_t *topk_idx, float *topk_score, int32_t *num_selected,
+                           void *workspace, size_t workspace_bytes, void *stream);
+
+/* Thread-local description of the last non-OK status on this thread. */
+const char *ml2_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ML2_H */

@@ -1,0 +1,275 @@
+// Selection of the k best accepted candidates (ML2Tuner Section 2: the
+// explorer keeps the highest predicted performance among the configurations
+// model V accepts, until (alpha+1)*N are held).
+//
+// Every included candidate i (mask set, score not NaN) gets a unique 64-bit
+// key   (ord(score) << 32) | (0xFFFFFFFF - i)
+// where ord maps float32 to uint32 monotonically (-0.0 first canonicalised to
+// +0.0).  Larger keys are better: higher score, then lower index.  The k-th
+// largest key is found by a most-significant-digit radix select (12-bit
+// digits; each pass histograms the candidates that still match the chosen
+// prefix and fixes one more digit), stopping as soon as the threshold bucket
+// holds exactly the number still needed.  A final pass gathers the keys above
+// the threshold (exactly min(k, #included) of them) and one workgroup sorts
+// them (bitonic, in LDS).  Every pass is launched unconditionally and exits at
+// once when the selection is already complete, so the host never waits.
+#include <math.h>
+
+#include "ml2_internal.h"
+
+namespace ml2 {
+namespace {
+
+constexpr int kDigitBits = 12;
+constexpr int kBins = 1 << kDigitBits;
+constexpr int kPasses = 6;  // 5 x 12 + 4 bits
+constexpr int kSortThreads = 1024;
+constexpr size_t kStateBytes = 256;
+constexpr size_t kHistBytes = kBins * sizeof(uint32_t);
+
+struct TopkState {
+  unsigned long long prefix;  // decided high bits of the threshold key
+  int nbits;                  // how many high bits are decided
+  int need;                   // keys still to take among those matching prefix
+  int done;                   // selection criterion complete
+  int total;                  // included candidates
+  int count;                  // gathered keys
+  int k;
+};
+
+__device__ __forceinline__ bool included(const uint8_t *valid, const float *scores, int64_t i,
+                                         float *s) {
+  if (valid && valid[i] == 0) return false;
+  *s = scores[i];
+  return !isnan(*s);
+}
+
+__device__ __forceinline__ unsigned long long make_key(float s, int64_t i) {
+  uint32_t b = __float_as_uint(s);
+  if (b == 0x80000000u) b = 0u;
+  const uint32_t ord = (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+  return ((unsigned long long)ord << 32) | (unsigned long long)(0xFFFFFFFFu - (uint32_t)i);
+}
+
+__global__ void topk_init(TopkState *st, uint32_t *hist, int32_t k, int64_t n) {
+  for (int b = threadIdx.x; b < kBins; b += blockDim.x) hist[b] = 0;
+  if (threadIdx.x == 0) {
+    st->prefix = 0;
+    st->nbits = 0;
+    st->need = k;
+    st->done = (k == 0 || n == 0) ? 1 : 0;
+    st->total = 0;
+    st->count = 0;
+    st->k = k;
+  }
+}
+
+// Histogram of the next digit over candidates matching the decided prefix.
+__global__ void __launch_bounds__(256) topk_hist(const uint8_t *valid, const float *scores,
+                                                 int64_t n, const TopkState *st, uint32_t *hist) {
+  __shared__ uint32_t h[kBins];
+  if (st->done) return;
+  const int nbits = st->nbits;
+  const unsigned long long prefix = st->prefix;
+  const int w = min(kDigitBits, 64 - nbits);
+  const int shift = 64 - nbits - w;
+  const unsigned long long dmask = (1ull << w) - 1ull;
+  for (int b = threadIdx.x; b < kBins; b += blockDim.x) h[b] = 0;
+  __syncthreads();
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    float s;
+    if (!included(valid, scores, i, &s)) continue;
+    const unsigned long long key = make_key(s, i);
+    if (nbits > 0 && (key >> (64 - nbits)) != prefix) continue;
+    atomicAdd(&h[(key >> shift) & dmask], 1u);
+  }
+  __syncthreads();
+  for (int b = threadIdx.x; b < kBins; b += blockDim.x)
+    if (h[b]) atomicAdd(&hist[b], h[b]);
+}
+
+// One workgroup: pick the digit holding the need-th largest key, update the
+// state, clear the histogram for the next pass.
+__global__ void __launch_bounds__(256) topk_pick(TopkState *st, uint32_t *hist, int pass) {
+  __shared__ uint32_t part[256];
+  __shared__ int total_s;
+  if (st->done) return;
+  const int nbits = st->nbits;
+  const int w = min(kDigitBits, 64 - nbits);
+  const int nb = 1 << w;
+  const int per = (nb + 255) / 256;  // bins per thread, from the top down
+  const int t = threadIdx.x;
+  // thread t owns bins [nb - (t+1)*per, nb - t*per) (the highest bins first)
+  uint32_t sum = 0;
+  for (int j = 0; j < per; ++j) {
+    const int b = nb - 1 - (t * per + j);
+    if (b >= 0) sum += hist[b];
+  }
+  part[t] = sum;
+  __syncthreads();
+  if (t == 0) {
+    uint32_t tot = 0;
+    for (int j = 0; j < 256; ++j) tot += part[j];
+    total_s = (int)tot;
+  }
+  __syncthreads();
+  if (t == 0) {
+    int need = st->need;
+    if (pass == 0) {
+      st->total = total_s;
+      if (total_s <= need) {  // everything included is selected
+        st->need = total_s;
+        st->done = 1;
+        need = -1;
+      }
+    }
+    if (need > 0) {
+      uint32_t cum = 0;
+      int owner = 0;
+      for (; owner < 256; ++owner) {
+        if (cum + part[owner] >= (uint32_t)need) break;
+        cum += part[owner];
+      }
+      int chosen = -1;
+      uint32_t inb = 0;
+      for (int j = 0; j < per; ++j) {
+        const int b = nb - 1 - (owner * per + j);
+        if (b < 0) break;
+        if (cum + hist[b] >= (uint32_t)need) {
+          chosen = b;
+          inb = hist[b];
+          break;
+        }
+        cum += hist[b];
+      }
+      need -= (int)cum;
+      st->prefix = (nbits > 0 ? (st->prefix << w) : 0ull) | (unsigned long long)chosen;
+      st->nbits = nbits + w;
+      st->need = need;
+      if ((uint32_t)need == inb || nbits + w >= 64) st->done = 1;
+    }
+  }
+  __syncthreads();
+  for (int b = t; b < kBins; b += blockDim.x) hist[b] = 0;
+}
+
+// Gather every included key whose decided high bits are >= the prefix.
+__global__ void __launch_bounds__(256) topk_gather(const uint8_t *valid, const float *scores,
+                                                   int64_t n, TopkState *st,
+                                                   unsigned long long *cand) {
+  const int k = st->k;
+  if (k == 0) return;
+  const int nbits = st->nbits;
+  const unsigned long long prefix = st->prefix;
+  const int lane = threadIdx.x & 63;
+  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const int64_t start = (int64_t)blockIdx.x * blockDim.x;
+  for (int64_t base = start; base < n; base += stride) {  // uniform trip count per wave
+    const int64_t i = base + threadIdx.x;
+    bool take = false;
+    unsigned long long key = 0;
+    float s;
+    if (i < n && included(valid, scores, i, &s)) {
+      key = make_key(s, i);
+      take = (nbits == 0) || ((key >> (64 - nbits)) >= prefix);
+    }
+    const uint64_t bal = __ballot(take);
+    if (bal == 0) continue;
+    int pos0 = 0;
+    if (lane == 0) pos0 = atomicAdd(&st->count, __popcll(bal));
+    pos0 = __shfl(pos0, 0);
+    if (take) {
+      const int pos = pos0 + __popcll(bal & below);
+      if (pos < k) cand[pos] = key;
+    }
+  }
+}
+
+// One workgroup: sort the gathered keys descending and write the outputs.
+__global__ void __launch_bounds__(kSortThreads) topk_sort(const float *scores, TopkState *st,
+                                                          const unsigned long long *cand,
+                                                          int32_t *idx, float *out,
+                                                          int32_t *num) {
+  extern __shared__ unsigned long long keys[];
+  const int k = st->k;
+  const int cnt = min(st->count, k);
+  int size = 1;
+  while (size < cnt) size <<= 1;
+  for (int j = threadIdx.x; j < size; j += blockDim.x) keys[j] = (j < cnt) ? cand[j] : 0ull;
+  __syncthreads();
+  for (int len = 2; len <= size; len <<= 1) {
+    for (int stride = len >> 1; stride > 0; stride >>= 1) {
+      for (int j = threadIdx.x; j < size; j += blockDim.x) {
+        const int p = j ^ stride;
+        if (p > j) {
+          const unsigned long long a = keys[j], b = keys[p];
+          const bool desc = (j & len) == 0;
+          if (desc ? (a < b) : (a > b)) {
+            keys[j] = b;
+            keys[p] = a;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  for (int j = threadIdx.x; j < k; j += blockDim.x) {
+    if (j < cnt) {
+      const int32_t i = (int32_t)(0xFFFFFFFFu - (uint32_t)(keys[j] & 0xFFFFFFFFull));
+      idx[j] = i;
+      out[j] = scores[i];
+    } else {
+      idx[j] = -1;
+      out[j] = -INFINITY;
+    }
+  }
+  if (threadIdx.x == 0) *num = cnt;
+}
+
+}  // namespace
+
+size_t topk_workspace_bytes(int64_t n, int32_t k) {
+  (void)n;
+  const size_t cand = (size_t)(k > 0 ? k : 1) * sizeof(unsigned long long);
+  return (kStateBytes + kHistBytes + cand + 255) & ~(size_t)255;
+}
+
+hipError_t launch_topk(const uint8_t *valid, const float *scores, int64_t n, int32_t k,
+                       int32_t *idx, float *score, int32_t *num, void *ws, int cu_count,
+                       hipStream_t s) {
+  char *w = static_cast<char *>(ws);
+  TopkState *st = reinterpret_cast<TopkState *>(w);
+  uint32_t *hist = reinterpret_cast<uint32_t *>(w + kStateBytes);
+  unsigned long long *cand = reinterpret_cast<unsigned long long *>(w + kStateBytes + kHistBytes);
+  hipLaunchKernelGGL(topk_init, dim3(1), dim3(256), 0, s, st, hist, k, n);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  int64_t blocks = (n + 255) / 256;
+  const int64_t cap = (int64_t)cu_count * 4;
+  if (blocks > cap) blocks = cap;
+  if (blocks < 1) blocks = 1;
+  if (n > 0 && k > 0) {
+    for (int pass = 0; pass < kPasses; ++pass) {
+      hipLaunchKernelGGL(topk_hist, dim3((unsigned)blocks), dim3(256), 0, s, valid, scores, n,
+                         st, hist);
+      hipLaunchKernelGGL(topk_pick, dim3(1), dim3(256), 0, s, st, hist, pass);
+    }
+    hipLaunchKernelGGL(topk_gather, dim3((unsigned)blocks), dim3(256), 0, s, valid, scores, n,
+                       st, cand);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  int size = 1;
+  while (size < k) size <<= 1;
+  const size_t lds = (size_t)size * sizeof(unsigned long long);
+  e = hipFuncSetAttribute(reinterpret_cast<const void *>(&topk_sort),
+                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(topk_sort, dim3(1), dim3(kSortThreads), lds, s, scores, st, cand, idx,
+                     score, num);
+  return hipGetLastError();
+}
+
+}  // namespace ml2

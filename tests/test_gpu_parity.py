@@ -1,0 +1,344 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Masks, top-k indices and scores must be bit-identical to the oracle (the
+fold order is fixed, so scores are expected at 0 ulp; the accepted bar for
+scores is |gpu - oracle| <= 1e-5 * max(|oracle|, 1), and anything above
+0 ulp is reported).  Inputs are seeded and synthetic.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+
+import gen
+import oracle
+from tests.treeutil import ensemble_from_trees, random_ragged_ensemble
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+from paper_2411_10764_amd import ml2  # noqa: E402
+
+DEV = "cuda:0"
+THREADS = gen.default_threads()
+
+
+def _note(msg):
+    print(f"[gpu-parity] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+def _to_dev(X, ld=None, offset=0):
+    """Device copy of X with row stride ld (>= F) and the first row `offset`
+    floats into the allocation (offset 1 breaks 16-byte alignment)."""
+    n, F = X.shape
+    ld = F if ld is None else ld
+    buf = torch.full((offset + n * ld + 4,), float("nan"), dtype=torch.float32, device=DEV)
+    view = buf[offset:offset + n * ld].view(n, ld) if n else buf[offset:offset].view(0, ld)
+    if n:
+        view[:, :F] = torch.from_numpy(np.ascontiguousarray(X)).to(DEV)
+    return view
+
+
+def run_gpu(V, P, X, k, ld=None, offset=0, perf_mask=True):
+    n = X.shape[0]
+    Xd = _to_dev(X, ld, offset)
+    v = ml2.ml2_load_ensemble(V)
+    p = ml2.ml2_load_ensemble(P)
+    valid = torch.empty(max(n, 1), dtype=torch.uint8, device=DEV)
+    margin = torch.empty(max(n, 1), dtype=torch.float32, device=DEV)
+    score = torch.empty(max(n, 1), dtype=torch.float32, device=DEV)
+    idx = torch.empty(max(k, 1), dtype=torch.int32, device=DEV)
+    top = torch.empty(max(k, 1), dtype=torch.float32, device=DEV)
+    num = torch.full((1,), -7, dtype=torch.int32, device=DEV)
+    wsb = ml2.ml2_topk_workspace_bytes(n, k)
+    ws = torch.empty(wsb, dtype=torch.uint8, device=DEV)
+    ml2.ml2_score_validity(v, Xd, valid, margin)
+    ml2.ml2_score_perf(p, Xd, valid if perf_mask else None, score)
+    ml2.ml2_filter_topk(valid if perf_mask else None, score, k, idx, top, num, ws, wsb, n)
+    torch.cuda.synchronize()
+    out = dict(valid=valid.cpu().numpy()[:n], margin=margin.cpu().numpy()[:n],
+               score=score.cpu().numpy()[:n], idx=idx.cpu().numpy()[:k],
+               top=top.cpu().numpy()[:k], num=int(num.item()))
+    v.free()
+    p.free()
+    return out
+
+
+def assert_scores(got, want, what):
+    same = (got.view(np.uint32) == want.view(np.uint32)) | (np.isnan(got) & np.isnan(want))
+    if not np.all(same):
+        bad = np.flatnonzero(~same)
+        tol = 1e-5 * np.maximum(np.abs(want[bad].astype(np.float64)), 1.0)
+        err = np.abs(got[bad].astype(np.float64) - want[bad].astype(np.float64))
+        _note(f"{what}: {bad.size} entries differ from the oracle above 0 ulp "
+              f"(max abs err {err.max():.3g})")
+        assert np.all(err <= tol), f"{what}: {int((err > tol).sum())} entries beyond 1e-5 rel"
+
+
+def check_pipeline(V, P, X, k, **kw):
+    got = run_gpu(V, P, X, k, **kw)
+    perf_mask = kw.get("perf_mask", True)
+    valid, margin = oracle.validity(V, X, THREADS)
+    score = oracle.perf(P, X, valid if perf_mask else None, THREADS)
+    idx, top, num = oracle.topk(valid if perf_mask else None, score, k)
+    assert np.array_equal(got["valid"], valid), "validity mask differs"
+    assert_scores(got["margin"], margin, "margin")
+    assert_scores(got["score"], score, "score")
+    assert got["num"] == num
+    assert np.array_equal(got["idx"], idx), "top-k indices differ"
+    assert np.array_equal(got["top"].view(np.uint32), top.view(np.uint32)), "top-k scores differ"
+    return got
+
+
+# ---- the workloads ---------------------------------------------------------------
+
+@pytest.mark.parametrize("name", ["tiny", "medium"])
+def test_workload_exact(name):
+    w = gen.WORKLOADS[name]
+    _note(f"{name}: n={w.n} F={w.F} V={w.v_trees}x{w.v_depth} P={w.p_trees}x{w.p_depth} k={w.k}")
+    X = w.features()
+    got = check_pipeline(w.validity(), w.perf(), X, w.k)
+    _note(f"{name}: invalid fraction {1 - got['valid'].mean():.4f}, top-k exact")
+
+
+def test_golden_hand_pipeline():
+    import json
+    import os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "hand_pipeline.json")))
+
+    def tree(node):
+        return (int(node[0]), float(node[1]), tree(node[2]), tree(node[3])) \
+            if isinstance(node, list) else float(node)
+
+    V = ensemble_from_trees([tree(t) for t in g["validity"]["trees"]], 3, g["validity"]["base"])
+    P = ensemble_from_trees([tree(t) for t in g["perf"]["trees"]], 3, g["perf"]["base"])
+    X = np.array([[float(v) for v in r] for r in g["candidates"]], np.float32)
+    for k in ("2", "5", "0"):
+        got = run_gpu(V, P, X, int(k))
+        e = g["expected"]
+        assert np.array_equal(got["margin"], np.array(e["margin"], np.float32))
+        assert np.array_equal(got["valid"], np.array(e["valid"], np.uint8))
+        assert np.array_equal(got["score"], np.array([float(s) for s in e["score"]], np.float32))
+        assert got["num"] == e["topk"][k]["num"]
+        assert got["idx"].tolist() == e["topk"][k]["idx"]
+
+
+def test_order_witness():
+    import json
+    import os
+    cases = json.load(open(os.path.join(os.path.dirname(__file__), "golden",
+                                        "order_witness.json")))["cases"]
+    for c in cases:
+        V = ensemble_from_trees([float(v) for v in c["leaves"]], 1, c["base"])
+        got = run_gpu(V, V, np.zeros((70, 1), np.float32), 3)
+        assert np.all(got["margin"] == np.float32(c["margin"]))
+        assert np.all(got["valid"] == c["valid"])
+
+
+# ---- ragged trees, special values, shapes ------------------------------------------
+
+def _special_features(rng, n, F, K):
+    X = np.empty((n, F), np.float32)
+    X[:, :K] = rng.integers(0, 9, size=(n, K))
+    X[:, K:] = np.exp(rng.normal(0, 1, size=(n, F - K)))
+    r = rng.random((n, F))
+    X[r < 0.03] = np.nan
+    X[(r >= 0.03) & (r < 0.05)] = -0.0
+    X[(r >= 0.05) & (r < 0.06)] = np.float32(2.0 ** -140)        # subnormal
+    X[(r >= 0.06) & (r < 0.07)] = np.inf
+    X[(r >= 0.07) & (r < 0.08)] = -np.inf
+    return X
+
+
+def _thr_sampler(K):
+    def f(r, feat):
+        u = r.random()
+        if u < 0.05:
+            return float(2.0 ** -140)
+        if u < 0.08:
+            return 0.0
+        if u < 0.10:
+            return float("inf")
+        return float(r.integers(0, 9)) if feat < K else float(np.float32(np.exp(r.normal())))
+    return f
+
+
+@pytest.mark.parametrize("seed,n,F,depth,trees", [
+    (1, 1, 5, 3, 3), (2, 63, 7, 5, 17), (3, 64, 16, 6, 9), (4, 65, 33, 7, 30),
+    (5, 257, 64, 9, 12), (6, 5000, 40, 4, 41), (7, 3000, 96, 10, 6), (8, 700, 128, 8, 25),
+])
+def test_ragged_trees_and_special_values(seed, n, F, depth, trees):
+    rng = np.random.default_rng(seed)
+    K = F // 2
+    V = random_ragged_ensemble(rng, trees, depth, F, _thr_sampler(K),
+                               lambda r: float(np.float32(r.normal(0, 0.5))), p_split=0.8,
+                               base=float(np.float32(rng.normal(0, 0.3))))
+    P = random_ragged_ensemble(rng, trees + 3, depth, F, _thr_sampler(K),
+                               lambda r: float(np.float32(r.normal(0, 0.1))), p_split=0.8)
+    X = _special_features(rng, n, F, K)
+    _note(f"ragged seed={seed} n={n} F={F} depth<={depth}")
+    check_pipeline(V, P, X, min(n, 37))
+
+
+@pytest.mark.parametrize("ld,offset", [(None, 0), (70, 0), (64, 1), (67, 3)])
+def test_strides_and_alignment(ld, offset):
+    w = gen.WORKLOADS["tiny"]
+    X = w.features()[:1000]
+    _note(f"stride ld={ld} offset={offset}")
+    check_pipeline(w.validity(), w.perf(), X, 50, ld=ld, offset=offset)
+
+
+@pytest.mark.parametrize("depth,F,trees", [(1, 1, 5), (1, 256, 40), (11, 8, 3), (12, 256, 2),
+                                           (6, 256, 33)])
+def test_depth_and_width_limits(depth, F, trees):
+    V = gen.perfect_ensemble(21, 1, trees, depth, F, F // 2, 0.5)
+    P = gen.perfect_ensemble(21, 2, trees, depth, F, F // 2, 0.1)
+    X = gen.features(21, 1500, F, F // 2)
+    _note(f"limits depth={depth} F={F} trees={trees}")
+    check_pipeline(V, P, X, 100)
+
+
+def test_perf_without_mask():
+    w = gen.WORKLOADS["tiny"]
+    check_pipeline(w.validity(), w.perf(), w.features(), 64, perf_mask=False)
+
+
+def test_empty_pool():
+    w = gen.WORKLOADS["tiny"]
+    got = run_gpu(w.validity(), w.perf(), np.zeros((0, w.F), np.float32), 5)
+    assert got["num"] == 0 and got["idx"].tolist() == [-1] * 5
+    assert np.all(got["top"] == -np.inf)
+
+
+# ---- selection edge cases ----------------------------------------------------------
+
+def _topk_gpu(valid, score, k):
+    n = score.shape[0]
+    s = torch.from_numpy(score).to(DEV) if n else torch.empty(1, device=DEV)
+    v = torch.from_numpy(valid).to(DEV) if valid is not None and n else None
+    idx = torch.empty(max(k, 1), dtype=torch.int32, device=DEV)
+    top = torch.empty(max(k, 1), dtype=torch.float32, device=DEV)
+    num = torch.full((1,), -7, dtype=torch.int32, device=DEV)
+    wsb = ml2.ml2_topk_workspace_bytes(n, k)
+    ws = torch.empty(wsb, dtype=torch.uint8, device=DEV)
+    ml2.ml2_filter_topk(v, s, k, idx, top, num, ws, wsb, n)
+    torch.cuda.synchronize()
+    return idx.cpu().numpy()[:k], top.cpu().numpy()[:k], int(num.item())
+
+
+def _check_topk(valid, score, k):
+    gi, gt, gn = _topk_gpu(valid, score, k)
+    oi, ot, on = oracle.topk(valid, score, k)
+    assert gn == on
+    assert np.array_equal(gi, oi)
+    assert np.array_equal(gt.view(np.uint32), ot.view(np.uint32))
+
+
+@pytest.mark.parametrize("case", ["constant", "dups", "signed_zero", "nan", "few_valid",
+                                  "k_zero", "k_max", "no_mask", "all_invalid", "extremes"])
+def test_topk_edge_cases(case):
+    rng = np.random.default_rng(sum(map(ord, case)))
+    n, k = 100000, 300
+    score = rng.normal(0, 1, n).astype(np.float32)
+    valid = (rng.random(n) < 0.5).astype(np.uint8)
+    if case == "constant":
+        score[:] = 0.75
+    elif case == "dups":
+        score = (rng.integers(0, 5, n) * 0.5).astype(np.float32)
+    elif case == "signed_zero":
+        score[:] = 0.0
+        score[rng.random(n) < 0.5] = -0.0
+    elif case == "nan":
+        score[rng.random(n) < 0.3] = np.nan
+    elif case == "few_valid":
+        valid[:] = 0
+        valid[rng.choice(n, 17, replace=False)] = 1
+    elif case == "k_zero":
+        k = 0
+    elif case == "k_max":
+        k = ml2.ML2_MAX_TOPK
+    elif case == "no_mask":
+        valid = None
+    elif case == "all_invalid":
+        valid[:] = 0
+    elif case == "extremes":
+        score[rng.random(n) < 0.2] = -np.inf
+        score[rng.random(n) < 0.2] = np.inf
+        score[rng.random(n) < 0.1] = np.float32(1e-45)
+    _check_topk(valid, score, k)
+
+
+@pytest.mark.parametrize("n", [1, 2, 255, 256, 257, 4096, 1 << 20])
+def test_topk_sizes(n):
+    rng = np.random.default_rng(n)
+    score = rng.normal(0, 1, n).astype(np.float32)
+    valid = (rng.random(n) < 0.7).astype(np.uint8)
+    for k in (1, 33, 1024):
+        _check_topk(valid, score, k)
+
+
+def test_repeatable_across_streams():
+    w = gen.WORKLOADS["medium"]
+    X = torch.from_numpy(w.features()).to(DEV)
+    v, p = ml2.ml2_load_ensemble(w.validity()), ml2.ml2_load_ensemble(w.perf())
+    outs = []
+    for s in (torch.cuda.Stream(), torch.cuda.current_stream()):
+        with torch.cuda.stream(s):
+            pipe = ml2.Pipeline(v, p, w.n, w.k, device=DEV, with_margin=True)
+            pipe.run(X)
+        s.synchronize()
+        outs.append([t.cpu().numpy().copy() for t in (pipe.valid, pipe.margin, pipe.score,
+                                                      pipe.idx, pipe.top, pipe.num)])
+    for a, b in zip(*outs):
+        assert np.array_equal(a.view(np.uint8), b.view(np.uint8))
+
+
+# ---- full-size workloads: sampled outputs + properties -----------------------------
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name", ["large", "roofline", "skewed"])
+def test_full_size_sampled(name):
+    w = gen.WORKLOADS[name]
+    _note(f"{name}: generating {w.n} x {w.F} features on the host")
+    X = w.features()
+    V, P = w.validity(), w.perf()
+    Xd = torch.from_numpy(X).to(DEV)
+    v, p = ml2.ml2_load_ensemble(V), ml2.ml2_load_ensemble(P)
+    pipe = ml2.Pipeline(v, p, w.n, w.k, device=DEV, with_margin=True)
+    _note(f"{name}: running the GPU pipeline")
+    pipe.run(Xd)
+    torch.cuda.synchronize()
+    valid = pipe.valid.cpu().numpy()
+    margin = pipe.margin.cpu().numpy()
+    score = pipe.score.cpu().numpy()
+    idx = pipe.idx.cpu().numpy()[: w.k]
+    top = pipe.top.cpu().numpy()[: w.k]
+    num = int(pipe.num.item())
+    del Xd
+    rng = np.random.default_rng(w.seed)
+    rows = np.unique(np.concatenate([rng.choice(w.n, 40000, replace=False),
+                                     np.arange(0, 70), np.arange(w.n - 70, w.n),
+                                     idx[idx >= 0]])).astype(np.int64)
+    _note(f"{name}: oracle on {rows.size} sampled rows")
+    Xs = X[rows]
+    ov, om = oracle.validity(V, Xs, THREADS)
+    os_ = oracle.perf(P, Xs, ov, THREADS)
+    assert np.array_equal(valid[rows], ov), "validity mask differs on sampled rows"
+    assert_scores(margin[rows], om, "margin (sampled)")
+    assert_scores(score[rows], os_, "score (sampled)")
+    # top-k properties over the whole pool (the selected rows were checked above)
+    n_valid = int(valid.sum())
+    assert num == min(w.k, n_valid)
+    sel = idx[:num]
+    assert len(set(sel.tolist())) == num and np.all(valid[sel] == 1)
+    assert np.array_equal(top[:num].view(np.uint32), score[sel].view(np.uint32))
+    keys = [(-float(score[i]), int(i)) for i in sel]
+    assert keys == sorted(keys)
+    last_s, last_i = float(score[sel[-1]]), int(sel[-1])
+    better = (valid == 1) & ((score > last_s) | ((score == last_s) & (np.arange(w.n) <= last_i)))
+    assert int(better.sum()) == num, "a better valid candidate was left out"
+    _note(f"{name}: invalid fraction {1 - n_valid / w.n:.4f}; sampled rows exact; top-{w.k} ok")
+    v.free()
+    p.free()
