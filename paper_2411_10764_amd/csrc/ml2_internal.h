@@ -44,6 +44,7 @@ struct WalkPlan {
   int waves;        // waves per workgroup; each wave owns 64 candidates
   int group;        // trees walked concurrently per lane (ILP)
   int chunk_trees;  // trees per LDS chunk (multiple of group)
+  int nbuf;         // chunk buffers: 2 (double-buffered) or 1
   size_t lds_bytes; // dynamic LDS per workgroup
   int grid;         // workgroups
 };

@@ -41,6 +41,7 @@ struct WalkArgs {
   int32_t nchunks;
   int32_t F;
   int32_t vec4;         // rows are 16-byte aligned (X aligned, ld % 4 == 0)
+  int32_t nbuf;         // 2: double-buffered chunks; 1: one buffer (deep trees, wide F)
   float base;
   uint8_t *valid_out;   // validity
   float *margin_out;
@@ -125,14 +126,19 @@ __device__ __forceinline__ float walk_all(const WalkArgs &a, char *buf0, char *b
   wait_all_and_barrier();
   float m = a.base;
   for (int c = 0; c < a.nchunks; ++c) {
-    if (c + 1 < a.nchunks) {
-      const int nt = min(a.chunk_trees, a.ntrees - (c + 1) * a.chunk_trees);
+    const bool more = c + 1 < a.nchunks;
+    const int nt = more ? min(a.chunk_trees, a.ntrees - (c + 1) * a.chunk_trees) : 0;
+    if (more && a.nbuf == 2)
       stage_async(a.trees + (size_t)(c + 1) * chunk_bytes, (c & 1) ? buf0 : buf1,
                   (uint32_t)nt * RB, wave, nwaves, lane);
-    }
     const int ntr = min(a.chunk_trees, a.ntrees - c * a.chunk_trees);
     m = walk_chunk<D, G>((c & 1) ? buf1 : buf0, ntr, tile_lane, m);
     wait_all_and_barrier();
+    if (more && a.nbuf == 1) {  // buf1 aliases buf0: refill after everyone is done
+      stage_async(a.trees + (size_t)(c + 1) * chunk_bytes, buf0, (uint32_t)nt * RB, wave,
+                  nwaves, lane);
+      wait_all_and_barrier();
+    }
   }
   return m;
 }
@@ -147,7 +153,7 @@ __global__ void __launch_bounds__(kLanes *kMaxWaves) validity_kernel(WalkArgs a)
   const size_t tile_bytes = (size_t)a.F * kTileStride;
   const uint32_t chunk_bytes = (uint32_t)a.chunk_trees * RB;
   char *buf0 = smem + W * tile_bytes;
-  char *buf1 = buf0 + chunk_bytes;
+  char *buf1 = buf0 + (a.nbuf == 2 ? chunk_bytes : 0u);
   char *tile_lane = smem + wave * tile_bytes + 4 * lane;
   const int64_t ntiles = (a.n + kLanes - 1) / kLanes;
   for (int64_t tg = blockIdx.x; tg * W < ntiles; tg += gridDim.x) {
@@ -175,7 +181,7 @@ __global__ void __launch_bounds__(kLanes *kMaxWaves) perf_kernel(WalkArgs a) {
   const size_t tile_bytes = (size_t)a.F * kTileStride;
   const uint32_t chunk_bytes = (uint32_t)a.chunk_trees * RB;
   char *buf0 = smem + W * tile_bytes;
-  char *buf1 = buf0 + chunk_bytes;
+  char *buf1 = buf0 + (a.nbuf == 2 ? chunk_bytes : 0u);
   int32_t *queue = reinterpret_cast<int32_t *>(buf1 + chunk_bytes);  // 2*B entries
   char *tile_lane = smem + wave * tile_bytes + 4 * lane;
   const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
@@ -270,6 +276,7 @@ WalkArgs make_args(const Forest &f, const WalkPlan &p, const float *X, int64_t n
   a.F = f.num_features;
   a.vec4 = ((reinterpret_cast<uintptr_t>(X) & 15u) == 0 && (ld & 3) == 0) ? 1 : 0;
   a.base = f.base;
+  a.nbuf = p.nbuf;
   return a;
 }
 
@@ -285,13 +292,15 @@ bool plan_walk(const Forest &f, int64_t n_work, int cu_count, WalkPlan *p, const
   const size_t chunk_bytes = (size_t)chunk_trees * rb;
   const size_t tile = (size_t)f.num_features * kTileStride;
   const size_t per_wave = tile + 2 * kLanes * sizeof(int32_t);  // tile + queue share
-  if (2 * chunk_bytes + per_wave > kLdsBudget) {
+  int nbuf = 2;
+  if (2 * chunk_bytes + per_wave > kLdsBudget) nbuf = 1;
+  if (nbuf * chunk_bytes + per_wave > kLdsBudget) {
     *why = "ensemble depth and feature count exceed the LDS of one workgroup";
     return false;
   }
-  int W = (int)((kLdsBudget - 2 * chunk_bytes) / per_wave);
+  int W = (int)((kLdsBudget - nbuf * chunk_bytes) / per_wave);
   if (W > 4) W = 4;
-  const size_t lds = (size_t)W * per_wave + 2 * chunk_bytes;
+  const size_t lds = (size_t)W * per_wave + nbuf * chunk_bytes;
   int per_cu = (int)(kLdsBudget / lds);
   if (per_cu < 1) per_cu = 1;
   if (per_cu > 8) per_cu = 8;
@@ -304,6 +313,7 @@ bool plan_walk(const Forest &f, int64_t n_work, int cu_count, WalkPlan *p, const
   p->group = G;
   p->chunk_trees = chunk_trees;
   p->lds_bytes = lds;
+  p->nbuf = nbuf;
   p->grid = (int)grid;
   return true;
 }
