@@ -116,46 +116,43 @@ ml2_status check_tree(const ml2_ensemble_desc &d, int32_t t, const TreeView &tv,
 }
 
 // Fill the perfect-tree record of depth D from the general tree (replicating
-// leaves that sit above depth D).
+// leaves that sit above depth D into dummy subtrees).
 void pad_tree(const TreeView &tv, int D, char *rec) {
-  const uint32_t ni = (1u << D) - 1u;
-  uint2 *nodes = reinterpret_cast<uint2 *>(rec);
-  float *leaves = reinterpret_cast<float *>(rec + 8u * ni);
+  const uint32_t L = 1u << D;
+  uint2 *nodes = reinterpret_cast<uint2 *>(rec);              // nodes[j], 1 <= j < L
+  float *leaves = reinterpret_cast<float *>(rec + 4u * L);    // leaves[j], L <= j < 2L
   struct Item {
     int32_t node;
     uint32_t pos;
-    int lvl;
   };
   std::vector<Item> stack;
-  stack.push_back({0, 0, 0});
+  stack.push_back({0, 1u});
   while (!stack.empty()) {
     const Item it = stack.back();
     stack.pop_back();
     const bool leaf = tv.left[it.node] == -1 && tv.right[it.node] == -1;
-    if (it.lvl == D) {  // only leaves reach depth D
-      leaves[it.pos - ni] = tv.val[it.node];
+    if (it.pos >= L) {  // only leaves reach depth D
+      leaves[it.pos] = tv.val[it.node];
       continue;
     }
     if (leaf) {
       nodes[it.pos] = make_uint2(0u, 0u);  // feature 0, threshold +0: both sides equal
-      stack.push_back({it.node, 2 * it.pos + 1, it.lvl + 1});
-      stack.push_back({it.node, 2 * it.pos + 2, it.lvl + 1});
+      stack.push_back({it.node, 2 * it.pos});
+      stack.push_back({it.node, 2 * it.pos + 1});
     } else {
       uint32_t tb;
       memcpy(&tb, &tv.thr[it.node], 4);
-      nodes[it.pos] = make_uint2((uint32_t)tv.feat[it.node], tb);
-      stack.push_back({tv.left[it.node], 2 * it.pos + 1, it.lvl + 1});
-      stack.push_back({tv.right[it.node], 2 * it.pos + 2, it.lvl + 1});
+      nodes[it.pos] = make_uint2((uint32_t)tv.feat[it.node] * ml2::kTileRowBytes, tb);
+      stack.push_back({tv.left[it.node], 2 * it.pos + 1});
+      stack.push_back({tv.right[it.node], 2 * it.pos});
     }
   }
 }
 
 void pad_identity_tree(int D, char *rec) {  // every leaf -0.0
-  const uint32_t ni = (1u << D) - 1u;
-  uint2 *nodes = reinterpret_cast<uint2 *>(rec);
-  float *leaves = reinterpret_cast<float *>(rec + 8u * ni);
-  for (uint32_t i = 0; i < ni; ++i) nodes[i] = make_uint2(0u, 0u);
-  for (uint32_t j = 0; j <= ni; ++j) leaves[j] = -0.0f;
+  const uint32_t L = 1u << D;
+  float *leaves = reinterpret_cast<float *>(rec + 4u * L);
+  for (uint32_t j = L; j < 2 * L; ++j) leaves[j] = -0.0f;
 }
 
 ml2_status check_stream_args(const ml2_ensemble *e, const float *X, int64_t n, int64_t ld,
@@ -241,10 +238,14 @@ ml2_status ml2_load_ensemble(const ml2_ensemble_desc *desc, ml2_ensemble **out) 
     else
       pad_identity_tree(depth, rec);
   }
-  hipError_t e = hipMalloc(&f.d_trees, bytes);
-  if (e == hipErrorOutOfMemory) return fail(ML2_ERR_OUT_OF_MEMORY, "hipMalloc(%zu)", bytes);
+  // The tree table is followed by kTreeSlack zero bytes: chunk staging reads
+  // whole register sets, past the end of the last chunk.
+  hipError_t e = hipMalloc(&f.d_trees, bytes + ml2::kTreeSlack);
+  if (e == hipErrorOutOfMemory)
+    return fail(ML2_ERR_OUT_OF_MEMORY, "hipMalloc(%zu)", bytes + ml2::kTreeSlack);
   if (e != hipSuccess) return hip_fail(e, "hipMalloc");
-  e = hipMemcpy(f.d_trees, host.data(), bytes, hipMemcpyHostToDevice);
+  e = hipMemset(f.d_trees, 0, bytes + ml2::kTreeSlack);
+  if (e == hipSuccess) e = hipMemcpy(f.d_trees, host.data(), bytes, hipMemcpyHostToDevice);
   if (e != hipSuccess) {
     (void)hipFree(f.d_trees);
     return hip_fail(e, "hipMemcpy");

@@ -16,15 +16,20 @@ namespace ml2 {
 // trees whose leaves are -0.0 (x + (-0.0) == x for every float x, so the
 // fold is unchanged).
 //
-// Tree record (rec_bytes, 16-byte aligned), breadth-first, 0-based heap:
-//   node[i]  i in [0, 2^D - 1): uint2 {feature index, threshold bits}
-//   leaf[j]  j in [0, 2^D):     float, at byte 8 * (2^D - 1) + 4 * j
-// Children of node i are 2i+1 (taken iff x[feature] < threshold) and 2i+2.
-constexpr int kTreePad = 8;
+// Tree record (rec_bytes bytes, 16-byte aligned), 1-based heap of depth D,
+// with L = 2^D:
+//   node j, 1 <= j < L  at byte 8*j:      uint2 {feature * kTileRowBytes,
+//                                                threshold bits}
+//   leaf j, L <= j < 2L at byte 4*L + 4*j: float   (byte 8*L .. 12*L)
+// The children of node j are 2j+1, taken iff x[feature] < threshold, and 2j,
+// taken otherwise, so a walk moves with u <- 2u + [x < t].  Byte 0..7 is
+// unused.
+constexpr int kTreePad = 16;  // >= the largest trees-per-lane group
+constexpr uint32_t kTileRowBytes = 256;  // one feature of 64 candidates, float32
+constexpr size_t kTreeSlack = 128 * 1024;  // readable zero bytes after the tree table
 
 inline constexpr uint32_t record_bytes(int depth) {
-  const uint32_t ni = (1u << depth) - 1u;
-  const uint32_t raw = 8u * ni + 4u * (ni + 1u);
+  const uint32_t raw = 12u << depth;
   return (raw + 15u) & ~15u;
 }
 
@@ -44,7 +49,7 @@ struct WalkPlan {
   int waves;        // waves per workgroup; each wave owns 64 candidates
   int group;        // trees walked concurrently per lane (ILP)
   int chunk_trees;  // trees per LDS chunk (multiple of group)
-  int nbuf;         // chunk buffers: 2 (double-buffered) or 1
+  int nbuf;         // LDS chunk buffers: 2 (asynchronous refill) or 1
   size_t lds_bytes; // dynamic LDS per workgroup
   int grid;         // workgroups
 };

@@ -9,17 +9,22 @@
 //     features the lanes' current nodes test.
 //   * All lanes of a wave walk the same trees in lockstep (the trees are
 //     perfect), so at level l the wave touches only the 2^l breadth-ordered
-//     nodes of that level: reads are broadcast or conflict-free.
-//   * The ensemble streams through LDS in chunks of whole trees, double
-//     buffered with direct global->LDS loads (global_load_lds_dwordx4); the
-//     next chunk is in flight while the current one is walked.
-//   * Each lane walks `G` trees at once (independent dependency chains) and
-//     adds their leaves to its running margin in tree-index order, so the
-//     float32 left fold is exactly the one the definition prescribes.
+//     nodes of that level: reads are broadcast or nearly conflict-free.
+//   * The ensemble streams through one LDS buffer in chunks of whole trees.
+//     The next chunk is fetched into registers while the current one is
+//     walked, then written to LDS between two barriers.
+//   * Each lane walks G trees at once, as two halves offset by half a level:
+//     while one half waits for its node (or feature) reads, the other half
+//     issues its own.  Leaves are added to the running margin in tree-index
+//     order, so the float32 left fold is exactly the defined one.
+//   * Per level a walk costs two LDS reads (node, feature value) and four
+//     VALU instructions (node address, feature address, compare, and one
+//     add-with-carry that moves to child 2u + [x < t]).
 //   * The performance pass compacts the accepted candidates of the pool into
 //     an LDS queue (wave ballots + a workgroup prefix) and only ever walks
 //     full tiles of accepted candidates; rejected ones get -inf directly.
 #include <math.h>
+#include <stdlib.h>
 
 #include "ml2_internal.h"
 
@@ -27,9 +32,10 @@ namespace ml2 {
 namespace {
 
 constexpr int kLanes = 64;
-constexpr int kTileStride = kLanes * 4;  // bytes per feature row of a wave tile
 constexpr size_t kLdsBudget = 160 * 1024 - 256;  // headroom for static LDS
 constexpr int kMaxWaves = 8;
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 struct WalkArgs {
   const float *X;
@@ -41,7 +47,9 @@ struct WalkArgs {
   int32_t nchunks;
   int32_t F;
   int32_t vec4;         // rows are 16-byte aligned (X aligned, ld % 4 == 0)
-  int32_t nbuf;         // 2: double-buffered chunks; 1: one buffer (deep trees, wide F)
+  int32_t nbuf;         // LDS chunk buffers: 2 (asynchronous refill) or 1
+  int32_t regstage;     // one buffer: the next chunk is fetched into registers
+  int32_t rowpf;        // 1: rows load with load_row_batched (vec4, F % 4 == 0, F <= 128)
   float base;
   uint8_t *valid_out;   // validity
   float *margin_out;
@@ -49,128 +57,333 @@ struct WalkArgs {
   float *score_out;
 };
 
-typedef __attribute__((address_space(3))) void lds_void;
-
-// Issue the asynchronous copy of `bytes` (multiple of 16) from global src to
-// LDS dst; every wave takes 1 KiB segments round-robin.  Completion is
-// awaited with s_waitcnt vmcnt(0) followed by a workgroup barrier.
-__device__ __forceinline__ void stage_async(const char *src, char *dst, uint32_t bytes,
-                                            int wave, int nwaves, int lane) {
-  for (uint32_t seg = (uint32_t)wave * 1024u; seg < bytes; seg += (uint32_t)nwaves * 1024u) {
-    const uint32_t off = seg + (uint32_t)lane * 16u;
-    if (off < bytes)
-      __builtin_amdgcn_global_load_lds((const void *)(src + off), (lds_void *)(dst + seg), 16, 0, 0);
-  }
-}
-
-__device__ __forceinline__ void wait_all_and_barrier() {
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-}
-
-// Row `row` of X into the wave tile, transposed (dst = tile + 4*lane).
+// Row `row` of X into the wave tile, transposed (dst = tile + 4*lane).  The
+// pool is read once: non-temporal loads keep it from evicting the ensemble
+// from L2.
 __device__ __forceinline__ void load_row(const WalkArgs &a, int64_t row, char *dst) {
   const float *src = a.X + row * a.ld;
   int q = 0;
   if (a.vec4) {
     for (; q + 4 <= a.F; q += 4) {
-      const float4 v = *reinterpret_cast<const float4 *>(src + q);
-      *reinterpret_cast<float *>(dst + (q + 0) * kTileStride) = v.x;
-      *reinterpret_cast<float *>(dst + (q + 1) * kTileStride) = v.y;
-      *reinterpret_cast<float *>(dst + (q + 2) * kTileStride) = v.z;
-      *reinterpret_cast<float *>(dst + (q + 3) * kTileStride) = v.w;
+      const f32x4 v = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(src + q));
+      *reinterpret_cast<float *>(dst + (q + 0) * kTileRowBytes) = v.x;
+      *reinterpret_cast<float *>(dst + (q + 1) * kTileRowBytes) = v.y;
+      *reinterpret_cast<float *>(dst + (q + 2) * kTileRowBytes) = v.z;
+      *reinterpret_cast<float *>(dst + (q + 3) * kTileRowBytes) = v.w;
     }
   }
-  for (; q < a.F; ++q) *reinterpret_cast<float *>(dst + q * kTileStride) = src[q];
+  for (; q < a.F; ++q)
+    *reinterpret_cast<float *>(dst + q * kTileRowBytes) = __builtin_nontemporal_load(src + q);
 }
+
+// Row `row` of X into the wave tile for pools of at most kRowVecs*4 features
+// with 16-byte aligned rows: every load is issued before the first LDS write
+// (one memory latency per round instead of one per vector).  Loads are
+// unconditional (a missing row reads row 0, a short row repeats its last
+// vector), so the compiler knows how many are in flight.
+constexpr int kRowVecs = 32;
+
+__device__ __forceinline__ void load_row_batched(const WalkArgs &a, int64_t row, char *dst) {
+  const int64_t rr = (row >= 0 && row < a.n) ? row : 0;
+  const f32x4 *src = reinterpret_cast<const f32x4 *>(a.X + rr * a.ld);
+  const int last = a.F / 4 - 1;
+  f32x4 v[kRowVecs];
+#pragma unroll
+  for (int k = 0; k < kRowVecs; ++k) v[k] = __builtin_nontemporal_load(src + min(k, last));
+#pragma unroll
+  for (int k = 0; k < kRowVecs; ++k) {
+    if (k <= last) {
+      *reinterpret_cast<float *>(dst + (4 * k + 0) * kTileRowBytes) = v[k].x;
+      *reinterpret_cast<float *>(dst + (4 * k + 1) * kTileRowBytes) = v[k].y;
+      *reinterpret_cast<float *>(dst + (4 * k + 2) * kTileRowBytes) = v[k].z;
+      *reinterpret_cast<float *>(dst + (4 * k + 3) * kTileRowBytes) = v[k].w;
+    }
+  }
+}
+
+// Tree chunks.  Chunk c holds trees [c*chunk_trees, min((c+1)*chunk_trees,
+// ntrees)) and is walked cyclically.  With two LDS buffers the next chunk is
+// copied by direct global->LDS loads (global_load_lds_dwordx4, no registers)
+// while the current one is walked; completion is awaited with
+// s_waitcnt vmcnt(0) and a workgroup barrier.  With one buffer the copy is
+// synchronous between two barriers.
+typedef __attribute__((address_space(3))) void lds_void;
+
+__device__ __forceinline__ uint32_t chunk_bytes_of(const WalkArgs &a, uint32_t rb, int c) {
+  const int nt = min(a.chunk_trees, a.ntrees - c * a.chunk_trees);
+  return (uint32_t)nt * rb;
+}
+
+__device__ __forceinline__ const char *chunk_src(const WalkArgs &a, uint32_t rb, int c) {
+  return a.trees + (size_t)c * a.chunk_trees * rb;
+}
+
+// Asynchronous copy of chunk c into dst: every wave takes 1 KiB segments.
+__device__ __forceinline__ void stage_async(const WalkArgs &a, uint32_t rb, int c, char *dst) {
+  const char *src = chunk_src(a, rb, c);
+  const uint32_t bytes = chunk_bytes_of(a, rb, c);
+  const uint32_t lane = threadIdx.x & (kLanes - 1);
+  const uint32_t nw = blockDim.x / kLanes;
+  for (uint32_t seg = (threadIdx.x / kLanes) * 1024u; seg < bytes; seg += nw * 1024u) {
+    const uint32_t off = seg + lane * 16u;
+    if (off < bytes)
+      __builtin_amdgcn_global_load_lds((const void *)(src + off), (lds_void *)(dst + seg), 16, 0,
+                                       0);
+  }
+}
+
+// Synchronous copy of chunk c into dst; caller synchronises.
+__device__ __forceinline__ void stage_copy(const WalkArgs &a, uint32_t rb, int c, char *dst) {
+  const uint4 *src = reinterpret_cast<const uint4 *>(chunk_src(a, rb, c));
+  uint4 *d = reinterpret_cast<uint4 *>(dst);
+  const uint32_t nv = chunk_bytes_of(a, rb, c) / 16u;
+  for (uint32_t i = threadIdx.x; i < nv; i += blockDim.x) d[i] = src[i];
+}
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+constexpr int kStageRegs = 6;  // 16-byte registers per thread for one chunk
+
+// One chunk in registers.  Loads are unconditional (the table has
+// kTreeSlack readable bytes after it), so the compiler knows how many are in
+// flight: writing one register set to LDS waits only for that set's loads,
+// not for those of the set loaded after it.
+__device__ __forceinline__ void stage_regs_load(const WalkArgs &a, uint32_t rb, int c,
+                                                u32x4 (&r)[kStageRegs]) {
+  const u32x4 *src = reinterpret_cast<const u32x4 *>(chunk_src(a, rb, c));
+#pragma unroll
+  for (int k = 0; k < kStageRegs; ++k) r[k] = src[threadIdx.x + (uint32_t)k * blockDim.x];
+}
+
+__device__ __forceinline__ void stage_regs_store(const WalkArgs &a, uint32_t rb, int c,
+                                                 const u32x4 (&r)[kStageRegs], char *dst) {
+  const uint32_t nv = chunk_bytes_of(a, rb, c) / 16u;
+  u32x4 *d = reinterpret_cast<u32x4 *>(dst);
+#pragma unroll
+  for (int k = 0; k < kStageRegs; ++k) {
+    const uint32_t i = threadIdx.x + (uint32_t)k * blockDim.x;
+    if (i < nv) d[i] = r[k];
+  }
+}
+
+__device__ __forceinline__ void wait_dma_and_barrier() {
+  __builtin_amdgcn_s_waitcnt(0);  // vmcnt(0): the direct-to-LDS copies have landed
+  __syncthreads();
+}
+
+// H walks of one half: heap positions u (1-based; children 2u, 2u+1),
+// current node {feature offset, threshold}, feature value and final leaf.
+template <int D, int H>
+struct Walks {
+  static constexpr uint32_t RB = record_bytes(D);
+  static constexpr uint32_t L = 1u << D;
+  uint32_t u[H];
+  uint2 nd[H];
+  float x[H];
+  float leaf[H];
+
+  __device__ __forceinline__ void start() {
+#pragma unroll
+    for (int g = 0; g < H; ++g) u[g] = 1u;
+  }
+  __device__ __forceinline__ void read_nodes(const char *rec) {
+#pragma unroll
+    for (int g = 0; g < H; ++g) nd[g] = *reinterpret_cast<const uint2 *>(rec + g * RB + 8u * u[g]);
+  }
+  __device__ __forceinline__ void read_features(const char *tile_lane) {
+#pragma unroll
+    for (int g = 0; g < H; ++g) x[g] = *reinterpret_cast<const float *>(tile_lane + nd[g].x);
+  }
+  // u <- 2u + [x < threshold]: one compare into a lane mask and one
+  // add-with-carry per walk.  All compares precede all adds, so each mask is
+  // H-1 instructions old when read (s_nop covers H < 3).
+  __device__ __forceinline__ void descend() {
+    uint64_t lt[H];
+#pragma unroll
+    for (int g = 0; g < H; ++g)
+      asm volatile("v_cmp_lt_f32_e64 %0, %1, %2"
+                   : "=s"(lt[g])
+                   : "v"(x[g]), "v"(__uint_as_float(nd[g].y)));
+    if (H < 3) asm volatile("s_nop 1");
+#pragma unroll
+    for (int g = 0; g < H; ++g)
+      asm volatile("v_addc_co_u32_e64 %0, vcc, %0, %0, %1" : "+v"(u[g]) : "s"(lt[g]) : "vcc");
+  }
+  __device__ __forceinline__ void read_leaves(const char *rec) {
+#pragma unroll
+    for (int g = 0; g < H; ++g)
+      leaf[g] = *reinterpret_cast<const float *>(rec + g * RB + 4u * L + 4u * u[g]);
+  }
+};
 
 // Walk `ntr` trees (a multiple of G) of the chunk at `cb`, folding their
 // leaves into m in tree order.
 template <int D, int G>
 __device__ __forceinline__ float walk_chunk(const char *cb, int ntr, const char *tile_lane,
                                             float m) {
-  constexpr uint32_t NI = (1u << D) - 1u;
   constexpr uint32_t RB = record_bytes(D);
-  for (int t0 = 0; t0 < ntr; t0 += G) {
-    const char *rec = cb + (uint32_t)t0 * RB;
-    uint32_t u[G];
+  if constexpr (G == 1) {
+    for (int t = 0; t < ntr; ++t) {
+      const char *rec = cb + (uint32_t)t * RB;
+      Walks<D, 1> A;
+      A.start();
 #pragma unroll
-    for (int g = 0; g < G; ++g) u[g] = 0;
+      for (int l = 0; l < D; ++l) {
+        A.read_nodes(rec);
+        A.read_features(tile_lane);
+        A.descend();
+      }
+      A.read_leaves(rec);
+      m = m + A.leaf[0];
+    }
+  } else {
+    constexpr int H = G / 2;
+    for (int t0 = 0; t0 < ntr; t0 += G) {
+      const char *recA = cb + (uint32_t)t0 * RB;
+      const char *recB = recA + H * RB;
+      Walks<D, H> A, B;
+      A.start();
+      B.start();
+      A.read_nodes(recA);
+      B.read_nodes(recB);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int l = 0; l < D; ++l) {
+      for (int l = 0; l < D; ++l) {
+        A.read_features(tile_lane);
+        __builtin_amdgcn_sched_barrier(0);
+        B.read_features(tile_lane);
+        __builtin_amdgcn_sched_barrier(0);
+        A.descend();
+        if (l + 1 < D) A.read_nodes(recA); else A.read_leaves(recA);
+        __builtin_amdgcn_sched_barrier(0);
+        B.descend();
+        if (l + 1 < D) B.read_nodes(recB); else B.read_leaves(recB);
+        __builtin_amdgcn_sched_barrier(0);
+      }
 #pragma unroll
-      for (int g = 0; g < G; ++g) {
-        const uint2 nd = *reinterpret_cast<const uint2 *>(rec + g * RB + u[g] * 8u);
-        const float x = *reinterpret_cast<const float *>(tile_lane + nd.x * (uint32_t)kTileStride);
-        u[g] = 2u * u[g] + ((x < __uint_as_float(nd.y)) ? 1u : 2u);
+      for (int g = 0; g < H; ++g) m = m + A.leaf[g];
+#pragma unroll
+      for (int g = 0; g < H; ++g) m = m + B.leaf[g];
+    }
+  }
+  return m;
+}
+
+// Staging state.  Invariant between walks: `cur` holds the chunk about to be
+// walked; the following chunk is in flight to `other` (two buffers) or to
+// the registers `r` (one buffer).
+struct Stage {
+  char *cur;    // holds the chunk about to be walked
+  char *other;  // two buffers: the next chunk lands here (== cur with one)
+  u32x4 ra[kStageRegs], rb[kStageRegs];  // one buffer: the next two chunks
+};
+
+__device__ __forceinline__ int cyc(const WalkArgs &a, int c) {
+  while (c >= a.nchunks) c -= a.nchunks;
+  return c;
+}
+
+__device__ __forceinline__ void stage_prime(const WalkArgs &a, uint32_t rb, Stage &s) {
+  stage_copy(a, rb, 0, s.cur);
+  if (a.nchunks > 1) {
+    if (a.nbuf == 2) {
+      stage_async(a, rb, 1, s.other);
+    } else if (a.regstage) {
+      stage_regs_load(a, rb, 1, s.ra);
+      stage_regs_load(a, rb, cyc(a, 2), s.rb);
+    }
+  }
+  wait_dma_and_barrier();
+}
+
+// After walking chunk c: make chunk c+1 (cyclically) current.  With
+// registers, `set` holds chunk c+1 and is refilled with chunk c+3.
+__device__ __forceinline__ void stage_advance(const WalkArgs &a, uint32_t rb, int c, Stage &s,
+                                              u32x4 (&set)[kStageRegs]) {
+  if (a.nchunks == 1) return;
+  const int next = cyc(a, c + 1);
+  if (a.nbuf == 2) {
+    wait_dma_and_barrier();  // chunk `next` landed; every wave is done with cur
+    char *t = s.cur;
+    s.cur = s.other;
+    s.other = t;
+    if (a.nchunks > 2) stage_async(a, rb, cyc(a, c + 2), s.other);
+  } else if (a.regstage) {
+    __syncthreads();  // every wave is done with the buffer
+    stage_regs_store(a, rb, next, set, s.cur);
+    stage_regs_load(a, rb, cyc(a, c + 3), set);
+    __syncthreads();
+  } else {
+    __syncthreads();
+    stage_copy(a, rb, next, s.cur);
+    __syncthreads();
+  }
+}
+
+// Every chunk of the ensemble for the candidates in the tiles; leaves the
+// staging invariant in place for the next round.
+template <int D, int G>
+__device__ __forceinline__ float walk_all(const WalkArgs &a, Stage &s, const char *tile_lane) {
+  constexpr uint32_t RB = record_bytes(D);
+  float m = a.base;
+  // Pairs of chunks, so that the register sets alternate statically; an odd
+  // chunk count leaves the sets swapped for the next round (fixed up below).
+  int c = 0;
+  for (; c + 1 < a.nchunks; c += 2) {
+    m = walk_chunk<D, G>(s.cur, (int)(chunk_bytes_of(a, RB, c) / RB), tile_lane, m);
+    stage_advance(a, RB, c, s, s.ra);
+    m = walk_chunk<D, G>(s.cur, (int)(chunk_bytes_of(a, RB, c + 1) / RB), tile_lane, m);
+    stage_advance(a, RB, c + 1, s, s.rb);
+  }
+  if (c < a.nchunks) {
+    m = walk_chunk<D, G>(s.cur, (int)(chunk_bytes_of(a, RB, c) / RB), tile_lane, m);
+    stage_advance(a, RB, c, s, s.ra);
+    if (a.regstage && a.nchunks > 1) {  // rb now holds the chunk after next: rotate
+#pragma unroll
+      for (int k = 0; k < kStageRegs; ++k) {
+        const u32x4 t = s.ra[k];
+        s.ra[k] = s.rb[k];
+        s.rb[k] = t;
       }
     }
-    float leaf[G];
-#pragma unroll
-    for (int g = 0; g < G; ++g)
-      leaf[g] = *reinterpret_cast<const float *>(rec + g * RB + 4u * NI + 4u * u[g]);
-#pragma unroll
-    for (int g = 0; g < G; ++g) m = m + leaf[g];
-  }
-  return m;
-}
-
-// All chunks of the ensemble for the candidates whose features are in the
-// tiles.  On entry chunk 0 has been issued into buf0 and the tiles written;
-// on exit every wave has passed the final barrier.
-template <int D, int G>
-__device__ __forceinline__ float walk_all(const WalkArgs &a, char *buf0, char *buf1,
-                                          uint32_t chunk_bytes, const char *tile_lane,
-                                          int wave, int nwaves, int lane) {
-  constexpr uint32_t RB = record_bytes(D);
-  wait_all_and_barrier();
-  float m = a.base;
-  for (int c = 0; c < a.nchunks; ++c) {
-    const bool more = c + 1 < a.nchunks;
-    const int nt = more ? min(a.chunk_trees, a.ntrees - (c + 1) * a.chunk_trees) : 0;
-    if (more && a.nbuf == 2)
-      stage_async(a.trees + (size_t)(c + 1) * chunk_bytes, (c & 1) ? buf0 : buf1,
-                  (uint32_t)nt * RB, wave, nwaves, lane);
-    const int ntr = min(a.chunk_trees, a.ntrees - c * a.chunk_trees);
-    m = walk_chunk<D, G>((c & 1) ? buf1 : buf0, ntr, tile_lane, m);
-    wait_all_and_barrier();
-    if (more && a.nbuf == 1) {  // buf1 aliases buf0: refill after everyone is done
-      stage_async(a.trees + (size_t)(c + 1) * chunk_bytes, buf0, (uint32_t)nt * RB, wave,
-                  nwaves, lane);
-      wait_all_and_barrier();
-    }
   }
   return m;
 }
 
 template <int D, int G>
-__global__ void __launch_bounds__(kLanes *kMaxWaves) validity_kernel(WalkArgs a) {
+__global__ void __launch_bounds__(kLanes *kMaxWaves) __attribute__((amdgpu_waves_per_eu(1, 1)))
+validity_kernel(WalkArgs a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   constexpr uint32_t RB = record_bytes(D);
   const int lane = threadIdx.x & (kLanes - 1);
   const int wave = threadIdx.x / kLanes;
   const int W = blockDim.x / kLanes;
-  const size_t tile_bytes = (size_t)a.F * kTileStride;
+  const size_t tile_bytes = (size_t)a.F * kTileRowBytes;
   const uint32_t chunk_bytes = (uint32_t)a.chunk_trees * RB;
-  char *buf0 = smem + W * tile_bytes;
-  char *buf1 = buf0 + (a.nbuf == 2 ? chunk_bytes : 0u);
+  Stage st;
+  st.cur = smem + W * tile_bytes;
+  st.other = st.cur + (a.nbuf == 2 ? chunk_bytes : 0u);
   char *tile_lane = smem + wave * tile_bytes + 4 * lane;
   const int64_t ntiles = (a.n + kLanes - 1) / kLanes;
+  stage_prime(a, RB, st);
   for (int64_t tg = blockIdx.x; tg * W < ntiles; tg += gridDim.x) {
     const int64_t row = (tg * W + wave) * kLanes + lane;
     const bool active = row < a.n;
-    stage_async(a.trees, buf0, (uint32_t)min(a.chunk_trees, a.ntrees) * RB, wave, W, lane);
-    if (active) load_row(a, row, tile_lane);
-    const float m = walk_all<D, G>(a, buf0, buf1, chunk_bytes, tile_lane, wave, W, lane);
+    if (a.rowpf)
+      load_row_batched(a, row, tile_lane);
+    else if (active)
+      load_row(a, row, tile_lane);
+    __syncthreads();
+    const float m = walk_all<D, G>(a, st, tile_lane);
     if (active) {
-      a.valid_out[row] = (m > 0.0f) ? 1 : 0;
-      if (a.margin_out) a.margin_out[row] = m;
+      __builtin_nontemporal_store((uint8_t)((m > 0.0f) ? 1 : 0), a.valid_out + row);
+      if (a.margin_out) __builtin_nontemporal_store(m, a.margin_out + row);
     }
   }
 }
 
 template <int D, int G>
-__global__ void __launch_bounds__(kLanes *kMaxWaves) perf_kernel(WalkArgs a) {
+__global__ void __launch_bounds__(kLanes *kMaxWaves) __attribute__((amdgpu_waves_per_eu(1, 1)))
+perf_kernel(WalkArgs a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   __shared__ int wave_count[kMaxWaves];
   constexpr uint32_t RB = record_bytes(D);
@@ -178,23 +391,26 @@ __global__ void __launch_bounds__(kLanes *kMaxWaves) perf_kernel(WalkArgs a) {
   const int wave = threadIdx.x / kLanes;
   const int B = blockDim.x;
   const int W = B / kLanes;
-  const size_t tile_bytes = (size_t)a.F * kTileStride;
+  const size_t tile_bytes = (size_t)a.F * kTileRowBytes;
   const uint32_t chunk_bytes = (uint32_t)a.chunk_trees * RB;
-  char *buf0 = smem + W * tile_bytes;
-  char *buf1 = buf0 + (a.nbuf == 2 ? chunk_bytes : 0u);
-  int32_t *queue = reinterpret_cast<int32_t *>(buf1 + chunk_bytes);  // 2*B entries
+  Stage st;
+  st.cur = smem + W * tile_bytes;
+  st.other = st.cur + (a.nbuf == 2 ? chunk_bytes : 0u);
+  int32_t *queue = reinterpret_cast<int32_t *>(st.other + chunk_bytes);  // 2*B entries
   char *tile_lane = smem + wave * tile_bytes + 4 * lane;
   const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   const int64_t nsteps = (a.n + B - 1) / B;
   int64_t step = blockIdx.x;
   int qn = 0;  // identical in every thread
-  for (;;) {
-    // Scan the mask B entries at a time until a full tile set is queued.
+  stage_prime(a, RB, st);
+  // Scan the mask B entries at a time until a full tile set is queued (or
+  // the pool is exhausted), then take up to B rows off the queue.
+  auto next_rows = [&]() -> int32_t {
     while (qn < B && step < nsteps) {
       const int64_t i = step * B + threadIdx.x;
       const bool in = i < a.n;
       const bool v = in && (a.valid_in == nullptr || a.valid_in[i] != 0);
-      if (in && !v) a.score_out[i] = -INFINITY;
+      if (in && !v) __builtin_nontemporal_store(-INFINITY, a.score_out + i);
       const uint64_t bal = __ballot(v);
       if (lane == 0) wave_count[wave] = __popcll(bal);
       __syncthreads();
@@ -209,29 +425,40 @@ __global__ void __launch_bounds__(kLanes *kMaxWaves) perf_kernel(WalkArgs a) {
       step += gridDim.x;
       __syncthreads();
     }
-    if (qn == 0) break;
     const int take = min(qn, B);
-    const int slot = threadIdx.x;
-    const int32_t row = (slot < take) ? queue[slot] : -1;
-    stage_async(a.trees, buf0, (uint32_t)min(a.chunk_trees, a.ntrees) * RB, wave, W, lane);
-    if (row >= 0) load_row(a, row, tile_lane);
-    const float m = walk_all<D, G>(a, buf0, buf1, chunk_bytes, tile_lane, wave, W, lane);
-    if (row >= 0) a.score_out[row] = m;
+    const int32_t r = (threadIdx.x < take) ? queue[threadIdx.x] : -1;
     const int rem = qn - take;
     const int32_t carry = (threadIdx.x < rem) ? queue[take + threadIdx.x] : 0;
     __syncthreads();
     if (threadIdx.x < rem) queue[threadIdx.x] = carry;
     qn = rem;
     __syncthreads();
+    return r;
+  };
+  for (;;) {
+    const int32_t row = next_rows();  // ends with a barrier
+    if (__syncthreads_or(row >= 0) == 0) break;
+    if (a.rowpf)
+      load_row_batched(a, row, tile_lane);
+    else if (row >= 0)
+      load_row(a, row, tile_lane);
+    __syncthreads();
+    const float m = walk_all<D, G>(a, st, tile_lane);
+    if (row >= 0) __builtin_nontemporal_store(m, a.score_out + row);
   }
 }
 
-constexpr int group_for_depth(int d) { return d <= 6 ? 8 : d <= 9 ? 4 : d <= 10 ? 2 : 1; }
+// Trees walked concurrently per lane that a depth allows (a chunk must hold
+// at least G whole trees in LDS).
+constexpr bool group_allowed(int d, int g) {
+  return d <= 7 ? (g == 8 || g == 16)
+       : d <= 9 ? (g == 4 || g == 8)
+       : d == 10 ? (g == 2 || g == 4)
+                 : (g == 1 || g == 2);
+}
 
-template <int D>
-hipError_t launch_depth(bool perf, const WalkPlan &p, const WalkArgs &a, hipStream_t s) {
-  constexpr int G = group_for_depth(D);
-  if (p.group != G) return hipErrorInvalidValue;
+template <int D, int G>
+hipError_t launch_dg(bool perf, const WalkPlan &p, const WalkArgs &a, hipStream_t s) {
   const void *fn = perf ? reinterpret_cast<const void *>(&perf_kernel<D, G>)
                         : reinterpret_cast<const void *>(&validity_kernel<D, G>);
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -243,6 +470,19 @@ hipError_t launch_depth(bool perf, const WalkPlan &p, const WalkArgs &a, hipStre
   else
     hipLaunchKernelGGL((validity_kernel<D, G>), grid, block, p.lds_bytes, s, a);
   return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_depth(bool perf, const WalkPlan &p, const WalkArgs &a, hipStream_t s) {
+  switch (p.group) {
+    case 1: if constexpr (group_allowed(D, 1)) return launch_dg<D, 1>(perf, p, a, s); break;
+    case 2: if constexpr (group_allowed(D, 2)) return launch_dg<D, 2>(perf, p, a, s); break;
+    case 4: if constexpr (group_allowed(D, 4)) return launch_dg<D, 4>(perf, p, a, s); break;
+    case 8: if constexpr (group_allowed(D, 8)) return launch_dg<D, 8>(perf, p, a, s); break;
+    case 16: if constexpr (group_allowed(D, 16)) return launch_dg<D, 16>(perf, p, a, s); break;
+    default: break;
+  }
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_walk(bool perf, const Forest &f, const WalkPlan &p, const WalkArgs &a,
@@ -264,6 +504,11 @@ hipError_t launch_walk(bool perf, const Forest &f, const WalkPlan &p, const Walk
   }
 }
 
+int env_int(const char *name, int dflt) {
+  const char *v = getenv(name);
+  return (v && *v) ? atoi(v) : dflt;
+}
+
 WalkArgs make_args(const Forest &f, const WalkPlan &p, const float *X, int64_t n, int64_t ld) {
   WalkArgs a{};
   a.X = X;
@@ -275,47 +520,76 @@ WalkArgs make_args(const Forest &f, const WalkPlan &p, const float *X, int64_t n
   a.nchunks = (f.num_trees_padded + p.chunk_trees - 1) / p.chunk_trees;
   a.F = f.num_features;
   a.vec4 = ((reinterpret_cast<uintptr_t>(X) & 15u) == 0 && (ld & 3) == 0) ? 1 : 0;
-  a.base = f.base;
   a.nbuf = p.nbuf;
+  a.regstage = (p.nbuf == 1 &&
+                (size_t)p.chunk_trees * f.rec_bytes <= (size_t)kStageRegs * 16 * kLanes * p.waves)
+                   ? 1 : 0;
+  a.rowpf = (a.vec4 && (f.num_features % 4) == 0 && f.num_features <= 4 * kRowVecs) ? 1 : 0;
+  a.base = f.base;
   return a;
 }
 
 }  // namespace
 
+// LDS of one workgroup = W candidate tiles (F * 256 bytes each, plus the
+// compaction queue share) + nbuf chunk buffers of chunk_trees whole trees
+// (a multiple of G, as large as the LDS allows).  ML2_WALK_GROUP /
+// ML2_WALK_WAVES / ML2_WALK_NBUF / ML2_WALK_CHUNK override the choice
+// (tuning sweeps); out-of-range overrides are ignored.
 bool plan_walk(const Forest &f, int64_t n_work, int cu_count, WalkPlan *p, const char **why) {
-  const int G = group_for_depth(f.depth);
+  const int D = f.depth;
   const size_t rb = f.rec_bytes;
-  int per = (int)(16384 / ((size_t)G * rb));
-  if (per < 1) per = 1;
-  int chunk_trees = G * per;
-  if (chunk_trees > f.num_trees_padded) chunk_trees = f.num_trees_padded;  // multiple of G
-  const size_t chunk_bytes = (size_t)chunk_trees * rb;
-  const size_t tile = (size_t)f.num_features * kTileStride;
-  const size_t per_wave = tile + 2 * kLanes * sizeof(int32_t);  // tile + queue share
-  int nbuf = 2;
-  if (2 * chunk_bytes + per_wave > kLdsBudget) nbuf = 1;
-  if (nbuf * chunk_bytes + per_wave > kLdsBudget) {
-    *why = "ensemble depth and feature count exceed the LDS of one workgroup";
-    return false;
+  const size_t tile = (size_t)f.num_features * kTileRowBytes;
+  const size_t per_wave = tile + 2 * kLanes * sizeof(int32_t);
+  const int want_g = env_int("ML2_WALK_GROUP", 0);
+  const int want_w = env_int("ML2_WALK_WAVES", 0);
+  const int want_b = env_int("ML2_WALK_NBUF", 0);
+  const int want_c = env_int("ML2_WALK_CHUNK", 0);
+  const int groups[5] = {16, 8, 4, 2, 1};
+  // Preference: four waves (one per SIMD); then one buffer refilled from
+  // registers, two buffers, one buffer copied synchronously; then larger G.
+  for (int need_w = 4; need_w >= 1; --need_w) {
+    for (int mode = 0; mode < 3; ++mode) {
+      const int nbuf = mode == 1 ? 2 : 1;
+      if (want_b && want_b != nbuf) continue;
+      for (int gi = 0; gi < 5; ++gi) {
+        const int G = groups[gi];
+        if (!group_allowed(D, G)) continue;
+        if (want_g && group_allowed(D, want_g) && G != want_g) continue;
+        int W = need_w;
+        if (want_w > 0) W = want_w;
+        if (W > kMaxWaves) continue;
+        if ((size_t)W * per_wave + (size_t)nbuf * G * rb > kLdsBudget) continue;
+        const size_t room = (kLdsBudget - (size_t)W * per_wave) / nbuf;
+        const int tpad = (f.num_trees_padded + G - 1) / G * G;
+        int chunk_trees = (int)(room / rb) / G * G;
+        if (mode == 0) {  // the chunk must fit the staging registers
+          const int reg_trees = (int)((size_t)kStageRegs * 16 * kLanes * W / rb) / G * G;
+          if (reg_trees < G) continue;
+          if (chunk_trees > reg_trees) chunk_trees = reg_trees;
+        }
+        if (want_c > 0 && want_c % G == 0 && want_c <= chunk_trees) chunk_trees = want_c;
+        if (chunk_trees > tpad) chunk_trees = tpad;
+        p->waves = W;
+        p->group = G;
+        p->chunk_trees = chunk_trees;
+        p->nbuf = nbuf;
+        p->lds_bytes = (size_t)W * per_wave + (size_t)nbuf * chunk_trees * rb;
+        int per_cu = (int)(kLdsBudget / p->lds_bytes);
+        if (per_cu < 1) per_cu = 1;
+        if (per_cu > 8) per_cu = 8;
+        const int64_t tiles = (n_work + kLanes - 1) / kLanes;
+        const int64_t wgs = (tiles + W - 1) / W;
+        int64_t grid = (int64_t)cu_count * per_cu;
+        if (wgs < grid) grid = wgs;
+        if (grid < 1) grid = 1;
+        p->grid = (int)grid;
+        return true;
+      }
+    }
   }
-  int W = (int)((kLdsBudget - nbuf * chunk_bytes) / per_wave);
-  if (W > 4) W = 4;
-  const size_t lds = (size_t)W * per_wave + nbuf * chunk_bytes;
-  int per_cu = (int)(kLdsBudget / lds);
-  if (per_cu < 1) per_cu = 1;
-  if (per_cu > 8) per_cu = 8;
-  const int64_t tiles = (n_work + kLanes - 1) / kLanes;
-  int64_t groups = (tiles + W - 1) / W;
-  int64_t grid = (int64_t)cu_count * per_cu;
-  if (groups < grid) grid = groups;
-  if (grid < 1) grid = 1;
-  p->waves = W;
-  p->group = G;
-  p->chunk_trees = chunk_trees;
-  p->lds_bytes = lds;
-  p->nbuf = nbuf;
-  p->grid = (int)grid;
-  return true;
+  *why = "ensemble depth and feature count exceed the LDS of one workgroup";
+  return false;
 }
 
 hipError_t launch_validity(const Forest &f, const WalkPlan &p, const float *X, int64_t n,
