@@ -49,7 +49,7 @@ struct WalkArgs {
   int32_t vec4;         // rows are 16-byte aligned (X aligned, ld % 4 == 0)
   int32_t nbuf;         // LDS chunk buffers: 2 (asynchronous refill) or 1
   int32_t regstage;     // one buffer: the next chunk is fetched into registers
-  int32_t rowpf;        // 1: rows load with load_row_batched (vec4, F % 4 == 0, F <= 128)
+  int32_t rowpf;        // 1: rows load in line batches (vec4, F % 4 == 0, F <= 128)
   float base;
   uint8_t *valid_out;   // validity
   float *margin_out;
@@ -76,28 +76,59 @@ __device__ __forceinline__ void load_row(const WalkArgs &a, int64_t row, char *d
     *reinterpret_cast<float *>(dst + q * kTileRowBytes) = __builtin_nontemporal_load(src + q);
 }
 
-// Row `row` of X into the wave tile for pools of at most kRowVecs*4 features
-// with 16-byte aligned rows: every load is issued before the first LDS write
-// (one memory latency per round instead of one per vector).  Loads are
-// unconditional (a missing row reads row 0, a short row repeats its last
-// vector), so the compiler knows how many are in flight.
+// Rows of pools with at most kRowVecs*4 features and 16-byte aligned rows
+// load in batches of 8 vectors, one 128-byte line per row and batch: a wave
+// then never has two requests for the same line in flight, which would
+// fetch the line again and evict the ensemble from L2.  The first batch of
+// the next round's rows is fetched while the current round is walked.
+// Loads are unconditional (a missing row reads row 0, a short row repeats
+// its last vector), so the compiler knows how many are in flight.
 constexpr int kRowVecs = 32;
+constexpr int kRowBatch = 8;
 
-__device__ __forceinline__ void load_row_batched(const WalkArgs &a, int64_t row, char *dst) {
+struct RowHead {
+  f32x4 v[kRowBatch];
+};
+
+__device__ __forceinline__ const f32x4 *row_src(const WalkArgs &a, int64_t row) {
   const int64_t rr = (row >= 0 && row < a.n) ? row : 0;
-  const f32x4 *src = reinterpret_cast<const f32x4 *>(a.X + rr * a.ld);
+  return reinterpret_cast<const f32x4 *>(a.X + rr * a.ld);
+}
+
+__device__ __forceinline__ void row_batch_load(const WalkArgs &a, int64_t row, int b,
+                                               f32x4 (&v)[kRowBatch]) {
+  const f32x4 *src = row_src(a, row);
   const int last = a.F / 4 - 1;
-  f32x4 v[kRowVecs];
 #pragma unroll
-  for (int k = 0; k < kRowVecs; ++k) v[k] = __builtin_nontemporal_load(src + min(k, last));
+  for (int k = 0; k < kRowBatch; ++k)
+    v[k] = __builtin_nontemporal_load(src + min(b * kRowBatch + k, last));
+}
+
+__device__ __forceinline__ void row_batch_store(const WalkArgs &a, int b,
+                                                const f32x4 (&v)[kRowBatch], char *dst) {
+  const int nv = a.F / 4;
 #pragma unroll
-  for (int k = 0; k < kRowVecs; ++k) {
-    if (k <= last) {
-      *reinterpret_cast<float *>(dst + (4 * k + 0) * kTileRowBytes) = v[k].x;
-      *reinterpret_cast<float *>(dst + (4 * k + 1) * kTileRowBytes) = v[k].y;
-      *reinterpret_cast<float *>(dst + (4 * k + 2) * kTileRowBytes) = v[k].z;
-      *reinterpret_cast<float *>(dst + (4 * k + 3) * kTileRowBytes) = v[k].w;
+  for (int k = 0; k < kRowBatch; ++k) {
+    const int q = b * kRowBatch + k;
+    if (q < nv) {
+      *reinterpret_cast<float *>(dst + (4 * q + 0) * kTileRowBytes) = v[k].x;
+      *reinterpret_cast<float *>(dst + (4 * q + 1) * kTileRowBytes) = v[k].y;
+      *reinterpret_cast<float *>(dst + (4 * q + 2) * kTileRowBytes) = v[k].z;
+      *reinterpret_cast<float *>(dst + (4 * q + 3) * kTileRowBytes) = v[k].w;
     }
+  }
+}
+
+// Write the row whose first batch is in `head` into the tile, loading the
+// remaining batches.
+__device__ __forceinline__ void row_commit(const WalkArgs &a, int64_t row, const RowHead &head,
+                                           char *dst) {
+  row_batch_store(a, 0, head.v, dst);
+  const int nb = (a.F / 4 + kRowBatch - 1) / kRowBatch;
+  for (int b = 1; b < nb; ++b) {
+    f32x4 v[kRowBatch];
+    row_batch_load(a, row, b, v);
+    row_batch_store(a, b, v, dst);
   }
 }
 
@@ -110,6 +141,7 @@ __device__ __forceinline__ void load_row_batched(const WalkArgs &a, int64_t row,
 typedef __attribute__((address_space(3))) void lds_void;
 
 __device__ __forceinline__ uint32_t chunk_bytes_of(const WalkArgs &a, uint32_t rb, int c) {
+  if (c >= a.nchunks) return 0u;  // padding chunk of the register-staged sequence
   const int nt = min(a.chunk_trees, a.ntrees - c * a.chunk_trees);
   return (uint32_t)nt * rb;
 }
@@ -142,6 +174,7 @@ __device__ __forceinline__ void stage_copy(const WalkArgs &a, uint32_t rb, int c
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kStageRegs = 6;  // 16-byte registers per thread for one chunk
+constexpr int kStageSets = 3;  // chunks in flight in registers (at most 4)
 
 // One chunk in registers.  Loads are unconditional (the table has
 // kTreeSlack readable bytes after it), so the compiler knows how many are in
@@ -149,7 +182,7 @@ constexpr int kStageRegs = 6;  // 16-byte registers per thread for one chunk
 // not for those of the set loaded after it.
 __device__ __forceinline__ void stage_regs_load(const WalkArgs &a, uint32_t rb, int c,
                                                 u32x4 (&r)[kStageRegs]) {
-  const u32x4 *src = reinterpret_cast<const u32x4 *>(chunk_src(a, rb, c));
+  const u32x4 *src = reinterpret_cast<const u32x4 *>(chunk_src(a, rb, c < a.nchunks ? c : 0));
 #pragma unroll
   for (int k = 0; k < kStageRegs; ++k) r[k] = src[threadIdx.x + (uint32_t)k * blockDim.x];
 }
@@ -274,11 +307,19 @@ __device__ __forceinline__ float walk_chunk(const char *cb, int ntr, const char 
 struct Stage {
   char *cur;    // holds the chunk about to be walked
   char *other;  // two buffers: the next chunk lands here (== cur with one)
-  u32x4 ra[kStageRegs], rb[kStageRegs];  // one buffer: the next two chunks
+  u32x4 r[kStageSets][kStageRegs];  // registers: the next kStageSets chunks
 };
 
-__device__ __forceinline__ int cyc(const WalkArgs &a, int c) {
-  while (c >= a.nchunks) c -= a.nchunks;
+// Length of the cyclic chunk sequence: with register staging it is padded
+// with empty chunks to a multiple of kStageSets, so that set j always holds
+// a chunk whose index is j+1 modulo kStageSets and every set index is a
+// compile-time constant.
+__device__ __forceinline__ int seq_len(const WalkArgs &a) {
+  return a.regstage ? (a.nchunks + kStageSets - 1) / kStageSets * kStageSets : a.nchunks;
+}
+
+__device__ __forceinline__ int cyc(int c, int nseq) {
+  while (c >= nseq) c -= nseq;
   return c;
 }
 
@@ -288,30 +329,36 @@ __device__ __forceinline__ void stage_prime(const WalkArgs &a, uint32_t rb, Stag
     if (a.nbuf == 2) {
       stage_async(a, rb, 1, s.other);
     } else if (a.regstage) {
-      stage_regs_load(a, rb, 1, s.ra);
-      stage_regs_load(a, rb, cyc(a, 2), s.rb);
+      const int nseq = seq_len(a);
+#pragma unroll
+      for (int j = 0; j < kStageSets; ++j) stage_regs_load(a, rb, cyc(1 + j, nseq), s.r[j]);
     }
   }
   wait_dma_and_barrier();
 }
 
-// After walking chunk c: make chunk c+1 (cyclically) current.  With
-// registers, `set` holds chunk c+1 and is refilled with chunk c+3.
-__device__ __forceinline__ void stage_advance(const WalkArgs &a, uint32_t rb, int c, Stage &s,
-                                              u32x4 (&set)[kStageRegs]) {
+// Register staging, after walking chunk c (c == J mod kStageSets): set J
+// holds chunk c+1; write it to LDS and start loading chunk c+1+kStageSets.
+// The sets loaded after set J stay in flight.
+template <int J>
+__device__ __forceinline__ void stage_advance_regs(const WalkArgs &a, uint32_t rb, int c,
+                                                   int nseq, Stage &s) {
+  __syncthreads();  // every wave is done with the buffer
+  stage_regs_store(a, rb, cyc(c + 1, nseq), s.r[J], s.cur);
+  stage_regs_load(a, rb, cyc(c + 1 + kStageSets, nseq), s.r[J]);
+  __syncthreads();
+}
+
+// Two buffers or a synchronous copy, after walking chunk c.
+__device__ __forceinline__ void stage_advance(const WalkArgs &a, uint32_t rb, int c, Stage &s) {
   if (a.nchunks == 1) return;
-  const int next = cyc(a, c + 1);
+  const int next = cyc(c + 1, a.nchunks);
   if (a.nbuf == 2) {
     wait_dma_and_barrier();  // chunk `next` landed; every wave is done with cur
     char *t = s.cur;
     s.cur = s.other;
     s.other = t;
-    if (a.nchunks > 2) stage_async(a, rb, cyc(a, c + 2), s.other);
-  } else if (a.regstage) {
-    __syncthreads();  // every wave is done with the buffer
-    stage_regs_store(a, rb, next, set, s.cur);
-    stage_regs_load(a, rb, cyc(a, c + 3), set);
-    __syncthreads();
+    if (a.nchunks > 2) stage_async(a, rb, cyc(c + 2, a.nchunks), s.other);
   } else {
     __syncthreads();
     stage_copy(a, rb, next, s.cur);
@@ -325,25 +372,25 @@ template <int D, int G>
 __device__ __forceinline__ float walk_all(const WalkArgs &a, Stage &s, const char *tile_lane) {
   constexpr uint32_t RB = record_bytes(D);
   float m = a.base;
-  // Pairs of chunks, so that the register sets alternate statically; an odd
-  // chunk count leaves the sets swapped for the next round (fixed up below).
-  int c = 0;
-  for (; c + 1 < a.nchunks; c += 2) {
-    m = walk_chunk<D, G>(s.cur, (int)(chunk_bytes_of(a, RB, c) / RB), tile_lane, m);
-    stage_advance(a, RB, c, s, s.ra);
-    m = walk_chunk<D, G>(s.cur, (int)(chunk_bytes_of(a, RB, c + 1) / RB), tile_lane, m);
-    stage_advance(a, RB, c + 1, s, s.rb);
-  }
-  if (c < a.nchunks) {
-    m = walk_chunk<D, G>(s.cur, (int)(chunk_bytes_of(a, RB, c) / RB), tile_lane, m);
-    stage_advance(a, RB, c, s, s.ra);
-    if (a.regstage && a.nchunks > 1) {  // rb now holds the chunk after next: rotate
+  if (a.nchunks == 1) return walk_chunk<D, G>(s.cur, a.ntrees, tile_lane, m);
+  if (a.regstage) {
+    const int nseq = seq_len(a);
+    for (int c = 0; c < nseq; c += kStageSets) {
 #pragma unroll
-      for (int k = 0; k < kStageRegs; ++k) {
-        const u32x4 t = s.ra[k];
-        s.ra[k] = s.rb[k];
-        s.rb[k] = t;
+      for (int j = 0; j < kStageSets; ++j) {
+        m = walk_chunk<D, G>(s.cur, (int)(chunk_bytes_of(a, RB, c + j) / RB), tile_lane, m);
+        switch (j) {  // compile-time set index
+          case 0: stage_advance_regs<0>(a, RB, c + j, nseq, s); break;
+          case 1: stage_advance_regs<1>(a, RB, c + j, nseq, s); break;
+          case 2: if constexpr (kStageSets > 2) stage_advance_regs<2>(a, RB, c + j, nseq, s); break;
+          default: if constexpr (kStageSets > 3) stage_advance_regs<3>(a, RB, c + j, nseq, s); break;
+        }
       }
+    }
+  } else {
+    for (int c = 0; c < a.nchunks; ++c) {
+      m = walk_chunk<D, G>(s.cur, (int)(chunk_bytes_of(a, RB, c) / RB), tile_lane, m);
+      stage_advance(a, RB, c, s);
     }
   }
   return m;
@@ -365,13 +412,17 @@ validity_kernel(WalkArgs a) {
   char *tile_lane = smem + wave * tile_bytes + 4 * lane;
   const int64_t ntiles = (a.n + kLanes - 1) / kLanes;
   stage_prime(a, RB, st);
+  RowHead head;
+  if (a.rowpf) row_batch_load(a, ((int64_t)blockIdx.x * W + wave) * kLanes + lane, 0, head.v);
   for (int64_t tg = blockIdx.x; tg * W < ntiles; tg += gridDim.x) {
     const int64_t row = (tg * W + wave) * kLanes + lane;
     const bool active = row < a.n;
-    if (a.rowpf)
-      load_row_batched(a, row, tile_lane);
-    else if (active)
+    if (a.rowpf) {
+      row_commit(a, row, head, tile_lane);
+      row_batch_load(a, ((tg + gridDim.x) * W + wave) * kLanes + lane, 0, head.v);
+    } else if (active) {
       load_row(a, row, tile_lane);
+    }
     __syncthreads();
     const float m = walk_all<D, G>(a, st, tile_lane);
     if (active) {
@@ -435,16 +486,20 @@ perf_kernel(WalkArgs a) {
     __syncthreads();
     return r;
   };
+  RowHead head;
+  int32_t row = next_rows();
+  if (a.rowpf) row_batch_load(a, row, 0, head.v);
   for (;;) {
-    const int32_t row = next_rows();  // ends with a barrier
     if (__syncthreads_or(row >= 0) == 0) break;
     if (a.rowpf)
-      load_row_batched(a, row, tile_lane);
+      row_commit(a, row, head, tile_lane);
     else if (row >= 0)
       load_row(a, row, tile_lane);
-    __syncthreads();
+    const int32_t nrow = next_rows();  // ends with a barrier: the tiles are complete
+    if (a.rowpf) row_batch_load(a, nrow, 0, head.v);
     const float m = walk_all<D, G>(a, st, tile_lane);
     if (row >= 0) __builtin_nontemporal_store(m, a.score_out + row);
+    row = nrow;
   }
 }
 
