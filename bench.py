@@ -32,8 +32,13 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-# VALU lane-issue ceiling of the chip: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz
+# VALU lane-instruction ceiling of the chip: 256 CUs x 4 SIMDs x 16 lanes x
+# 2.4 GHz (the fp32 vector peak of 157.3 TFLOP/s counts a packed FMA as 4).
 VALU_LANE_OPS_PER_S = 256 * 4 * 16 * 2.4e9
+# A node visit needs at least two VALU instructions: the comparison
+# x[feature] < threshold and the step to the chosen child.
+VALU_OPS_PER_VISIT = 2
+VISIT_PEAK_PER_S = VALU_LANE_OPS_PER_S / VALU_OPS_PER_VISIT
 METRIC = "candidate configs scored+filtered/sec (validity+perf+top-k); % of HBM peak"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "perf_walk_roofline_traffic.json")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2411_10764_amd", "csrc", "walk_kernels.hip")
@@ -170,19 +175,21 @@ def main() -> int:
     visits_p = n_valid * w.p_trees * w.p_depth
     sha = _kernel_sha()
     perf_visits_per_s = visits_p / (t_perf / 1000.0)
+    traffic = _traffic(sha) if w.name == "roofline" else None
     roofline = {
         "bound": "alu",
         "kernel": "perf_kernel (model P walk over accepted candidates)",
         "achieved": perf_visits_per_s / 1e12,
-        "peak": VALU_LANE_OPS_PER_S / 1e12,
+        "peak": VISIT_PEAK_PER_S / 1e12,
         "unit": "Tvisit/s",
-        "frac": perf_visits_per_s / VALU_LANE_OPS_PER_S,
-        "traffic": _traffic(sha),
+        "frac": perf_visits_per_s / VISIT_PEAK_PER_S,
+        "traffic": traffic,
+        "traffic_unit": "bytes per launch (HBM read + write, copy-calibrated rocprofv3 counters)",
         "work_per_launch": f"{visits_p} node visits ({n_valid} accepted x {w.p_trees} trees "
                            f"x depth {w.p_depth})",
         "launch_ms": t_perf,
         "validity_kernel": {"achieved": visits_v / (t_val / 1000.0) / 1e12, "launch_ms": t_val,
-                            "frac": visits_v / (t_val / 1000.0) / VALU_LANE_OPS_PER_S},
+                            "frac": visits_v / (t_val / 1000.0) / VISIT_PEAK_PER_S},
         "hbm": {"algorithmic_bytes_per_step": alg_bytes,
                 "achieved_gbs": alg_bytes / (ms_per_step / 1000.0) / 1e9,
                 "peak_gbs": HBM_PEAK_GBS,
