@@ -50,6 +50,11 @@ struct WalkArgs {
   int32_t nbuf;         // LDS chunk buffers: 2 (asynchronous refill) or 1
   int32_t regstage;     // one buffer: the next chunk is fetched into registers
   int32_t rowpf;        // 1: rows load in line batches (vec4, F % 4 == 0, F <= 128)
+  int32_t nthreads;     // threads per workgroup (== blockDim.x).  Read from the
+                        // kernel arguments, which stay in scalar registers;
+                        // blockDim.x is a vector load from the dispatch packet
+                        // that the compiler re-issues under register pressure,
+                        // and each re-issue waits for every load in flight.
   float base;
   uint8_t *valid_out;   // validity
   float *margin_out;
@@ -155,7 +160,7 @@ __device__ __forceinline__ void stage_async(const WalkArgs &a, uint32_t rb, int 
   const char *src = chunk_src(a, rb, c);
   const uint32_t bytes = chunk_bytes_of(a, rb, c);
   const uint32_t lane = threadIdx.x & (kLanes - 1);
-  const uint32_t nw = blockDim.x / kLanes;
+  const uint32_t nw = a.nthreads / kLanes;
   for (uint32_t seg = (threadIdx.x / kLanes) * 1024u; seg < bytes; seg += nw * 1024u) {
     const uint32_t off = seg + lane * 16u;
     if (off < bytes)
@@ -169,12 +174,14 @@ __device__ __forceinline__ void stage_copy(const WalkArgs &a, uint32_t rb, int c
   const uint4 *src = reinterpret_cast<const uint4 *>(chunk_src(a, rb, c));
   uint4 *d = reinterpret_cast<uint4 *>(dst);
   const uint32_t nv = chunk_bytes_of(a, rb, c) / 16u;
-  for (uint32_t i = threadIdx.x; i < nv; i += blockDim.x) d[i] = src[i];
+  for (uint32_t i = threadIdx.x; i < nv; i += a.nthreads) d[i] = src[i];
 }
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kStageRegs = 6;  // 16-byte registers per thread for one chunk
-constexpr int kStageSets = 3;  // chunks in flight in registers (at most 4)
+// Chunks in flight in registers (2..4; four spill at the widest groups).
+constexpr int kValiditySets = 3;
+constexpr int kPerfSets = 3;
 
 // One chunk in registers.  Loads are unconditional (the table has
 // kTreeSlack readable bytes after it), so the compiler knows how many are in
@@ -184,7 +191,7 @@ __device__ __forceinline__ void stage_regs_load(const WalkArgs &a, uint32_t rb, 
                                                 u32x4 (&r)[kStageRegs]) {
   const u32x4 *src = reinterpret_cast<const u32x4 *>(chunk_src(a, rb, c < a.nchunks ? c : 0));
 #pragma unroll
-  for (int k = 0; k < kStageRegs; ++k) r[k] = src[threadIdx.x + (uint32_t)k * blockDim.x];
+  for (int k = 0; k < kStageRegs; ++k) r[k] = src[threadIdx.x + (uint32_t)k * a.nthreads];
 }
 
 __device__ __forceinline__ void stage_regs_store(const WalkArgs &a, uint32_t rb, int c,
@@ -193,7 +200,7 @@ __device__ __forceinline__ void stage_regs_store(const WalkArgs &a, uint32_t rb,
   u32x4 *d = reinterpret_cast<u32x4 *>(dst);
 #pragma unroll
   for (int k = 0; k < kStageRegs; ++k) {
-    const uint32_t i = threadIdx.x + (uint32_t)k * blockDim.x;
+    const uint32_t i = threadIdx.x + (uint32_t)k * a.nthreads;
     if (i < nv) d[i] = r[k];
   }
 }
@@ -304,18 +311,20 @@ __device__ __forceinline__ float walk_chunk(const char *cb, int ntr, const char 
 // Staging state.  Invariant between walks: `cur` holds the chunk about to be
 // walked; the following chunk is in flight to `other` (two buffers) or to
 // the registers `r` (one buffer).
+// K: chunks in flight in registers (2..4).
+template <int K>
 struct Stage {
   char *cur;    // holds the chunk about to be walked
   char *other;  // two buffers: the next chunk lands here (== cur with one)
-  u32x4 r[kStageSets][kStageRegs];  // registers: the next kStageSets chunks
+  u32x4 r[K][kStageRegs];  // registers: the next K chunks
 };
 
 // Length of the cyclic chunk sequence: with register staging it is padded
-// with empty chunks to a multiple of kStageSets, so that set j always holds
-// a chunk whose index is j+1 modulo kStageSets and every set index is a
-// compile-time constant.
+// with empty chunks to a multiple of K, so that set j always holds a chunk
+// whose index is j+1 modulo K and every set index is a compile-time constant.
+template <int K>
 __device__ __forceinline__ int seq_len(const WalkArgs &a) {
-  return a.regstage ? (a.nchunks + kStageSets - 1) / kStageSets * kStageSets : a.nchunks;
+  return a.regstage ? (a.nchunks + K - 1) / K * K : a.nchunks;
 }
 
 __device__ __forceinline__ int cyc(int c, int nseq) {
@@ -323,34 +332,37 @@ __device__ __forceinline__ int cyc(int c, int nseq) {
   return c;
 }
 
-__device__ __forceinline__ void stage_prime(const WalkArgs &a, uint32_t rb, Stage &s) {
+template <int K>
+__device__ __forceinline__ void stage_prime(const WalkArgs &a, uint32_t rb, Stage<K> &s) {
   stage_copy(a, rb, 0, s.cur);
   if (a.nchunks > 1) {
     if (a.nbuf == 2) {
       stage_async(a, rb, 1, s.other);
     } else if (a.regstage) {
-      const int nseq = seq_len(a);
+      const int nseq = seq_len<K>(a);
 #pragma unroll
-      for (int j = 0; j < kStageSets; ++j) stage_regs_load(a, rb, cyc(1 + j, nseq), s.r[j]);
+      for (int j = 0; j < K; ++j) stage_regs_load(a, rb, cyc(1 + j, nseq), s.r[j]);
     }
   }
   wait_dma_and_barrier();
 }
 
-// Register staging, after walking chunk c (c == J mod kStageSets): set J
-// holds chunk c+1; write it to LDS and start loading chunk c+1+kStageSets.
-// The sets loaded after set J stay in flight.
-template <int J>
+// Register staging, after walking chunk c (c == J mod K): set J holds chunk
+// c+1; write it to LDS and start loading chunk c+1+K.  The sets loaded after
+// set J stay in flight.
+template <int J, int K>
 __device__ __forceinline__ void stage_advance_regs(const WalkArgs &a, uint32_t rb, int c,
-                                                   int nseq, Stage &s) {
+                                                   int nseq, Stage<K> &s) {
   __syncthreads();  // every wave is done with the buffer
   stage_regs_store(a, rb, cyc(c + 1, nseq), s.r[J], s.cur);
-  stage_regs_load(a, rb, cyc(c + 1 + kStageSets, nseq), s.r[J]);
+  stage_regs_load(a, rb, cyc(c + 1 + K, nseq), s.r[J]);
   __syncthreads();
 }
 
 // Two buffers or a synchronous copy, after walking chunk c.
-__device__ __forceinline__ void stage_advance(const WalkArgs &a, uint32_t rb, int c, Stage &s) {
+template <int K>
+__device__ __forceinline__ void stage_advance(const WalkArgs &a, uint32_t rb, int c,
+                                              Stage<K> &s) {
   if (a.nchunks == 1) return;
   const int next = cyc(c + 1, a.nchunks);
   if (a.nbuf == 2) {
@@ -368,22 +380,22 @@ __device__ __forceinline__ void stage_advance(const WalkArgs &a, uint32_t rb, in
 
 // Every chunk of the ensemble for the candidates in the tiles; leaves the
 // staging invariant in place for the next round.
-template <int D, int G>
-__device__ __forceinline__ float walk_all(const WalkArgs &a, Stage &s, const char *tile_lane) {
+template <int D, int G, int K>
+__device__ __forceinline__ float walk_all(const WalkArgs &a, Stage<K> &s, const char *tile_lane) {
   constexpr uint32_t RB = record_bytes(D);
   float m = a.base;
   if (a.nchunks == 1) return walk_chunk<D, G>(s.cur, a.ntrees, tile_lane, m);
   if (a.regstage) {
-    const int nseq = seq_len(a);
-    for (int c = 0; c < nseq; c += kStageSets) {
+    const int nseq = seq_len<K>(a);
+    for (int c = 0; c < nseq; c += K) {
 #pragma unroll
-      for (int j = 0; j < kStageSets; ++j) {
+      for (int j = 0; j < K; ++j) {
         m = walk_chunk<D, G>(s.cur, (int)(chunk_bytes_of(a, RB, c + j) / RB), tile_lane, m);
         switch (j) {  // compile-time set index
-          case 0: stage_advance_regs<0>(a, RB, c + j, nseq, s); break;
-          case 1: stage_advance_regs<1>(a, RB, c + j, nseq, s); break;
-          case 2: if constexpr (kStageSets > 2) stage_advance_regs<2>(a, RB, c + j, nseq, s); break;
-          default: if constexpr (kStageSets > 3) stage_advance_regs<3>(a, RB, c + j, nseq, s); break;
+          case 0: stage_advance_regs<0, K>(a, RB, c + j, nseq, s); break;
+          case 1: stage_advance_regs<1, K>(a, RB, c + j, nseq, s); break;
+          case 2: if constexpr (K > 2) stage_advance_regs<2, K>(a, RB, c + j, nseq, s); break;
+          default: if constexpr (K > 3) stage_advance_regs<3, K>(a, RB, c + j, nseq, s); break;
         }
       }
     }
@@ -403,10 +415,10 @@ validity_kernel(WalkArgs a) {
   constexpr uint32_t RB = record_bytes(D);
   const int lane = threadIdx.x & (kLanes - 1);
   const int wave = threadIdx.x / kLanes;
-  const int W = blockDim.x / kLanes;
+  const int W = a.nthreads / kLanes;
   const size_t tile_bytes = (size_t)a.F * kTileRowBytes;
   const uint32_t chunk_bytes = (uint32_t)a.chunk_trees * RB;
-  Stage st;
+  Stage<kValiditySets> st;
   st.cur = smem + W * tile_bytes;
   st.other = st.cur + (a.nbuf == 2 ? chunk_bytes : 0u);
   char *tile_lane = smem + wave * tile_bytes + 4 * lane;
@@ -440,11 +452,11 @@ perf_kernel(WalkArgs a) {
   constexpr uint32_t RB = record_bytes(D);
   const int lane = threadIdx.x & (kLanes - 1);
   const int wave = threadIdx.x / kLanes;
-  const int B = blockDim.x;
+  const int B = a.nthreads;
   const int W = B / kLanes;
   const size_t tile_bytes = (size_t)a.F * kTileRowBytes;
   const uint32_t chunk_bytes = (uint32_t)a.chunk_trees * RB;
-  Stage st;
+  Stage<kPerfSets> st;
   st.cur = smem + W * tile_bytes;
   st.other = st.cur + (a.nbuf == 2 ? chunk_bytes : 0u);
   int32_t *queue = reinterpret_cast<int32_t *>(st.other + chunk_bytes);  // 2*B entries
@@ -580,6 +592,7 @@ WalkArgs make_args(const Forest &f, const WalkPlan &p, const float *X, int64_t n
                 (size_t)p.chunk_trees * f.rec_bytes <= (size_t)kStageRegs * 16 * kLanes * p.waves)
                    ? 1 : 0;
   a.rowpf = (a.vec4 && (f.num_features % 4) == 0 && f.num_features <= 4 * kRowVecs) ? 1 : 0;
+  a.nthreads = p.waves * kLanes;
   a.base = f.base;
   return a;
 }
