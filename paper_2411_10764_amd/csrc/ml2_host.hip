@@ -142,7 +142,7 @@ void pad_tree(const TreeView &tv, int D, char *rec) {
     } else {
       uint32_t tb;
       memcpy(&tb, &tv.thr[it.node], 4);
-      nodes[it.pos] = make_uint2((uint32_t)tv.feat[it.node] * ml2::kTileRowBytes, tb);
+      nodes[it.pos] = make_uint2((uint32_t)tv.feat[it.node], tb);
       stack.push_back({tv.left[it.node], 2 * it.pos + 1});
       stack.push_back({tv.right[it.node], 2 * it.pos});
     }

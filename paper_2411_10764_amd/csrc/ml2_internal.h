@@ -18,14 +18,12 @@ namespace ml2 {
 //
 // Tree record (rec_bytes bytes, 16-byte aligned), 1-based heap of depth D,
 // with L = 2^D:
-//   node j, 1 <= j < L  at byte 8*j:      uint2 {feature * kTileRowBytes,
-//                                                threshold bits}
+//   node j, 1 <= j < L  at byte 8*j:      uint2 {feature index, threshold bits}
 //   leaf j, L <= j < 2L at byte 4*L + 4*j: float   (byte 8*L .. 12*L)
 // The children of node j are 2j+1, taken iff x[feature] < threshold, and 2j,
 // taken otherwise, so a walk moves with u <- 2u + [x < t].  Byte 0..7 is
 // unused.
-constexpr int kTreePad = 16;  // >= the largest trees-per-lane group
-constexpr uint32_t kTileRowBytes = 256;  // one feature of 64 candidates, float32
+constexpr int kTreePad = 16;  // >= the trees of the largest walk group
 constexpr size_t kTreeSlack = 128 * 1024;  // readable zero bytes after the tree table
 
 inline constexpr uint32_t record_bytes(int depth) {
@@ -46,7 +44,9 @@ struct Forest {
 
 // Launch parameters of a walk (chosen on the host from D and F).
 struct WalkPlan {
-  int waves;        // waves per workgroup; each wave owns 64 candidates
+  int split;        // lanes per candidate: 1, or 2 (the two half-waves walk
+                    // alternate halves of every tree group)
+  int waves;        // waves per workgroup; each wave owns 64 / split candidates
   int group;        // trees walked concurrently per lane (ILP)
   int chunk_trees;  // trees per LDS chunk (multiple of group)
   int nbuf;         // LDS chunk buffers: 2 (asynchronous refill) or 1

@@ -3,15 +3,21 @@
 // configuration explorer (Section 2, "ML Model P" / "ML Model V").
 //
 // Mapping (one workgroup = W waves, persistent over the pool):
-//   * lane = candidate.  Each wave owns a tile of 64 candidates whose
-//     features sit in LDS transposed, feature f of lane l at f*256 + 4*l, so
-//     the per-level feature reads of a wave hit 64 distinct banks whatever
-//     features the lanes' current nodes test.
-//   * All lanes of a wave walk the same trees in lockstep (the trees are
-//     perfect), so at level l the wave touches only the 2^l breadth-ordered
-//     nodes of that level: reads are broadcast or nearly conflict-free.
+//   * Each wave owns a tile of 64/S candidates whose features sit in LDS
+//     transposed: feature f of candidate c at f * (256/S) + 4c, so the
+//     per-level feature reads of a wave hit distinct banks whatever features
+//     the lanes' current nodes test.
+//   * S = 1: lane = candidate.  S = 2: lanes c and c+32 hold candidate c; the
+//     lower half-wave walks the first G trees of every group of 2G, the upper
+//     half the next G, and the lower half folds both (the upper half's leaves
+//     cross over with one v_permlane32_swap per tree).  Splitting halves the
+//     tile of a wave, so twice as many waves fit the LDS and every SIMD runs
+//     two: one wave's VALU work issues while the other's LDS reads do.
+//   * All lanes of a half-wave walk the same trees in lockstep (the trees are
+//     perfect), so at level l a tree is touched only at its 2^l
+//     breadth-ordered nodes of that level.
 //   * The ensemble streams through one LDS buffer in chunks of whole trees.
-//     The next chunk is fetched into registers while the current one is
+//     The next chunks are fetched into registers while the current one is
 //     walked, then written to LDS between two barriers.
 //   * Each lane walks G trees at once, as two halves offset by half a level:
 //     while one half waits for its node (or feature) reads, the other half
@@ -36,6 +42,17 @@ constexpr size_t kLdsBudget = 160 * 1024 - 256;  // headroom for static LDS
 constexpr int kMaxWaves = 8;
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Tile geometry for S lanes per candidate.
+template <int S>
+struct Geo {
+  static constexpr int kCand = kLanes / S;            // candidates per wave
+  static constexpr uint32_t kRowBytes = 4u * kCand;   // one feature of a tile
+  static constexpr int kRowShift = S == 1 ? 8 : 7;    // log2(kRowBytes)
+  static constexpr int kStageRegs = 6 / S;            // 16-byte registers per
+                                                      // thread for one chunk
+};
 
 struct WalkArgs {
   const float *X;
@@ -62,32 +79,35 @@ struct WalkArgs {
   float *score_out;
 };
 
-// Row `row` of X into the wave tile, transposed (dst = tile + 4*lane).  The
-// pool is read once: non-temporal loads keep it from evicting the ensemble
-// from L2.
+// Row `row` of X into the tile of its candidate (dst = tile + 4*candidate),
+// whole, by one lane.  The pool is read once: non-temporal loads keep it from
+// evicting the ensemble from L2.
+template <int S>
 __device__ __forceinline__ void load_row(const WalkArgs &a, int64_t row, char *dst) {
+  constexpr uint32_t RW = Geo<S>::kRowBytes;
   const float *src = a.X + row * a.ld;
   int q = 0;
   if (a.vec4) {
     for (; q + 4 <= a.F; q += 4) {
       const f32x4 v = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(src + q));
-      *reinterpret_cast<float *>(dst + (q + 0) * kTileRowBytes) = v.x;
-      *reinterpret_cast<float *>(dst + (q + 1) * kTileRowBytes) = v.y;
-      *reinterpret_cast<float *>(dst + (q + 2) * kTileRowBytes) = v.z;
-      *reinterpret_cast<float *>(dst + (q + 3) * kTileRowBytes) = v.w;
+      *reinterpret_cast<float *>(dst + (q + 0) * RW) = v.x;
+      *reinterpret_cast<float *>(dst + (q + 1) * RW) = v.y;
+      *reinterpret_cast<float *>(dst + (q + 2) * RW) = v.z;
+      *reinterpret_cast<float *>(dst + (q + 3) * RW) = v.w;
     }
   }
   for (; q < a.F; ++q)
-    *reinterpret_cast<float *>(dst + q * kTileRowBytes) = __builtin_nontemporal_load(src + q);
+    *reinterpret_cast<float *>(dst + q * RW) = __builtin_nontemporal_load(src + q);
 }
 
 // Rows of pools with at most kRowVecs*4 features and 16-byte aligned rows
 // load in batches of 8 vectors, one 128-byte line per row and batch: a wave
 // then never has two requests for the same line in flight, which would
-// fetch the line again and evict the ensemble from L2.  The first batch of
-// the next round's rows is fetched while the current round is walked.
-// Loads are unconditional (a missing row reads row 0, a short row repeats
-// its last vector), so the compiler knows how many are in flight.
+// fetch the line again and evict the ensemble from L2.  With S lanes per
+// candidate, lane half h loads batches h, h+S, ...  The first batch of the
+// next round's rows is fetched while the current round is walked.  Loads are
+// unconditional (a missing row reads row 0, a short row repeats its last
+// vector), so the compiler knows how many are in flight.
 constexpr int kRowVecs = 32;
 constexpr int kRowBatch = 8;
 
@@ -109,31 +129,34 @@ __device__ __forceinline__ void row_batch_load(const WalkArgs &a, int64_t row, i
     v[k] = __builtin_nontemporal_load(src + min(b * kRowBatch + k, last));
 }
 
+template <int S>
 __device__ __forceinline__ void row_batch_store(const WalkArgs &a, int b,
                                                 const f32x4 (&v)[kRowBatch], char *dst) {
+  constexpr uint32_t RW = Geo<S>::kRowBytes;
   const int nv = a.F / 4;
 #pragma unroll
   for (int k = 0; k < kRowBatch; ++k) {
     const int q = b * kRowBatch + k;
     if (q < nv) {
-      *reinterpret_cast<float *>(dst + (4 * q + 0) * kTileRowBytes) = v[k].x;
-      *reinterpret_cast<float *>(dst + (4 * q + 1) * kTileRowBytes) = v[k].y;
-      *reinterpret_cast<float *>(dst + (4 * q + 2) * kTileRowBytes) = v[k].z;
-      *reinterpret_cast<float *>(dst + (4 * q + 3) * kTileRowBytes) = v[k].w;
+      *reinterpret_cast<float *>(dst + (4 * q + 0) * RW) = v[k].x;
+      *reinterpret_cast<float *>(dst + (4 * q + 1) * RW) = v[k].y;
+      *reinterpret_cast<float *>(dst + (4 * q + 2) * RW) = v[k].z;
+      *reinterpret_cast<float *>(dst + (4 * q + 3) * RW) = v[k].w;
     }
   }
 }
 
-// Write the row whose first batch is in `head` into the tile, loading the
-// remaining batches.
+// Write batch h of the row (already in `head`) and the lane half's further
+// batches h+S, h+2S, ... into the tile.
+template <int S>
 __device__ __forceinline__ void row_commit(const WalkArgs &a, int64_t row, const RowHead &head,
-                                           char *dst) {
-  row_batch_store(a, 0, head.v, dst);
+                                           int h, char *dst) {
+  row_batch_store<S>(a, h, head.v, dst);
   const int nb = (a.F / 4 + kRowBatch - 1) / kRowBatch;
-  for (int b = 1; b < nb; ++b) {
+  for (int b = h + S; b < nb; b += S) {
     f32x4 v[kRowBatch];
     row_batch_load(a, row, b, v);
-    row_batch_store(a, b, v, dst);
+    row_batch_store<S>(a, b, v, dst);
   }
 }
 
@@ -141,8 +164,9 @@ __device__ __forceinline__ void row_commit(const WalkArgs &a, int64_t row, const
 // ntrees)) and is walked cyclically.  With two LDS buffers the next chunk is
 // copied by direct global->LDS loads (global_load_lds_dwordx4, no registers)
 // while the current one is walked; completion is awaited with
-// s_waitcnt vmcnt(0) and a workgroup barrier.  With one buffer the copy is
-// synchronous between two barriers.
+// s_waitcnt vmcnt(0) and a workgroup barrier.  With one buffer the copy goes
+// through registers (loaded chunks ahead) or is synchronous between two
+// barriers.
 typedef __attribute__((address_space(3))) void lds_void;
 
 __device__ __forceinline__ uint32_t chunk_bytes_of(const WalkArgs &a, uint32_t rb, int c) {
@@ -177,29 +201,29 @@ __device__ __forceinline__ void stage_copy(const WalkArgs &a, uint32_t rb, int c
   for (uint32_t i = threadIdx.x; i < nv; i += a.nthreads) d[i] = src[i];
 }
 
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-constexpr int kStageRegs = 6;  // 16-byte registers per thread for one chunk
 // Chunks in flight in registers (2..4; four spill at the widest groups).
 constexpr int kValiditySets = 3;
 constexpr int kPerfSets = 3;
 
-// One chunk in registers.  Loads are unconditional (the table has
-// kTreeSlack readable bytes after it), so the compiler knows how many are in
-// flight: writing one register set to LDS waits only for that set's loads,
-// not for those of the set loaded after it.
+// One chunk in R registers per thread.  Loads are unconditional (the table
+// has kTreeSlack readable bytes after it), so the compiler knows how many are
+// in flight: writing one register set to LDS waits only for that set's
+// loads, not for those of the sets loaded after it.
+template <int R>
 __device__ __forceinline__ void stage_regs_load(const WalkArgs &a, uint32_t rb, int c,
-                                                u32x4 (&r)[kStageRegs]) {
+                                                u32x4 (&r)[R]) {
   const u32x4 *src = reinterpret_cast<const u32x4 *>(chunk_src(a, rb, c < a.nchunks ? c : 0));
 #pragma unroll
-  for (int k = 0; k < kStageRegs; ++k) r[k] = src[threadIdx.x + (uint32_t)k * a.nthreads];
+  for (int k = 0; k < R; ++k) r[k] = src[threadIdx.x + (uint32_t)k * a.nthreads];
 }
 
+template <int R>
 __device__ __forceinline__ void stage_regs_store(const WalkArgs &a, uint32_t rb, int c,
-                                                 const u32x4 (&r)[kStageRegs], char *dst) {
+                                                 const u32x4 (&r)[R], char *dst) {
   const uint32_t nv = chunk_bytes_of(a, rb, c) / 16u;
   u32x4 *d = reinterpret_cast<u32x4 *>(dst);
 #pragma unroll
-  for (int k = 0; k < kStageRegs; ++k) {
+  for (int k = 0; k < R; ++k) {
     const uint32_t i = threadIdx.x + (uint32_t)k * a.nthreads;
     if (i < nv) d[i] = r[k];
   }
@@ -210,9 +234,17 @@ __device__ __forceinline__ void wait_dma_and_barrier() {
   __syncthreads();
 }
 
+// Lanes 0..31 receive the value of lanes 32..63 (v_permlane32_swap: the
+// second result holds the first operand's upper half in its lower half).
+__device__ __forceinline__ float from_upper_half(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  return __uint_as_float(r[1]);
+}
+
 // H walks of one half: heap positions u (1-based; children 2u, 2u+1),
-// current node {feature offset, threshold}, feature value and final leaf.
-template <int D, int H>
+// current node {feature index, threshold}, feature value and final leaf.
+template <int D, int H, int S>
 struct Walks {
   static constexpr uint32_t RB = record_bytes(D);
   static constexpr uint32_t L = 1u << D;
@@ -231,7 +263,8 @@ struct Walks {
   }
   __device__ __forceinline__ void read_features(const char *tile_lane) {
 #pragma unroll
-    for (int g = 0; g < H; ++g) x[g] = *reinterpret_cast<const float *>(tile_lane + nd[g].x);
+    for (int g = 0; g < H; ++g)
+      x[g] = *reinterpret_cast<const float *>(tile_lane + (nd[g].x << Geo<S>::kRowShift));
   }
   // u <- 2u + [x < threshold]: one compare into a lane mask and one
   // add-with-carry per walk.  All compares precede all adds, so each mask is
@@ -253,18 +286,33 @@ struct Walks {
     for (int g = 0; g < H; ++g)
       leaf[g] = *reinterpret_cast<const float *>(rec + g * RB + 4u * L + 4u * u[g]);
   }
+  // Fold this half's leaves (lower lanes' own), in tree order.
+  __device__ __forceinline__ float fold(float m) const {
+#pragma unroll
+    for (int g = 0; g < H; ++g) m = m + leaf[g];
+    return m;
+  }
+  // Fold the upper half-wave's leaves into the lower half's margins.
+  __device__ __forceinline__ float fold_upper(float m) const {
+#pragma unroll
+    for (int g = 0; g < H; ++g) m = m + from_upper_half(leaf[g]);
+    return m;
+  }
 };
 
-// Walk `ntr` trees (a multiple of G) of the chunk at `cb`, folding their
-// leaves into m in tree order.
-template <int D, int G>
+// Walk `ntr` trees (a multiple of S*G) of the chunk at `cb`, folding their
+// leaves into m in tree order.  Half-wave h walks trees [t0 + h*G, t0 +
+// (h+1)*G) of each group of S*G; with S = 2 only the lower half's m is the
+// candidate's margin.
+template <int D, int G, int S>
 __device__ __forceinline__ float walk_chunk(const char *cb, int ntr, const char *tile_lane,
-                                            float m) {
+                                            int h, float m) {
   constexpr uint32_t RB = record_bytes(D);
+  constexpr int GS = G * S;
   if constexpr (G == 1) {
-    for (int t = 0; t < ntr; ++t) {
-      const char *rec = cb + (uint32_t)t * RB;
-      Walks<D, 1> A;
+    for (int t0 = 0; t0 < ntr; t0 += GS) {
+      const char *rec = cb + (uint32_t)(t0 + h) * RB;
+      Walks<D, 1, S> A;
       A.start();
 #pragma unroll
       for (int l = 0; l < D; ++l) {
@@ -273,14 +321,15 @@ __device__ __forceinline__ float walk_chunk(const char *cb, int ntr, const char 
         A.descend();
       }
       A.read_leaves(rec);
-      m = m + A.leaf[0];
+      m = A.fold(m);
+      if constexpr (S == 2) m = A.fold_upper(m);
     }
   } else {
     constexpr int H = G / 2;
-    for (int t0 = 0; t0 < ntr; t0 += G) {
-      const char *recA = cb + (uint32_t)t0 * RB;
+    for (int t0 = 0; t0 < ntr; t0 += GS) {
+      const char *recA = cb + (uint32_t)(t0 + h * G) * RB;
       const char *recB = recA + H * RB;
-      Walks<D, H> A, B;
+      Walks<D, H, S> A, B;
       A.start();
       B.start();
       A.read_nodes(recA);
@@ -299,10 +348,8 @@ __device__ __forceinline__ float walk_chunk(const char *cb, int ntr, const char 
         if (l + 1 < D) B.read_nodes(recB); else B.read_leaves(recB);
         __builtin_amdgcn_sched_barrier(0);
       }
-#pragma unroll
-      for (int g = 0; g < H; ++g) m = m + A.leaf[g];
-#pragma unroll
-      for (int g = 0; g < H; ++g) m = m + B.leaf[g];
+      m = B.fold(A.fold(m));
+      if constexpr (S == 2) m = B.fold_upper(A.fold_upper(m));
     }
   }
   return m;
@@ -311,12 +358,12 @@ __device__ __forceinline__ float walk_chunk(const char *cb, int ntr, const char 
 // Staging state.  Invariant between walks: `cur` holds the chunk about to be
 // walked; the following chunk is in flight to `other` (two buffers) or to
 // the registers `r` (one buffer).
-// K: chunks in flight in registers (2..4).
-template <int K>
+// K: chunks in flight in registers, R registers each.
+template <int K, int R>
 struct Stage {
   char *cur;    // holds the chunk about to be walked
   char *other;  // two buffers: the next chunk lands here (== cur with one)
-  u32x4 r[K][kStageRegs];  // registers: the next K chunks
+  u32x4 r[K][R];  // registers: the next K chunks
 };
 
 // Length of the cyclic chunk sequence: with register staging it is padded
@@ -332,8 +379,8 @@ __device__ __forceinline__ int cyc(int c, int nseq) {
   return c;
 }
 
-template <int K>
-__device__ __forceinline__ void stage_prime(const WalkArgs &a, uint32_t rb, Stage<K> &s) {
+template <int K, int R>
+__device__ __forceinline__ void stage_prime(const WalkArgs &a, uint32_t rb, Stage<K, R> &s) {
   stage_copy(a, rb, 0, s.cur);
   if (a.nchunks > 1) {
     if (a.nbuf == 2) {
@@ -341,7 +388,7 @@ __device__ __forceinline__ void stage_prime(const WalkArgs &a, uint32_t rb, Stag
     } else if (a.regstage) {
       const int nseq = seq_len<K>(a);
 #pragma unroll
-      for (int j = 0; j < K; ++j) stage_regs_load(a, rb, cyc(1 + j, nseq), s.r[j]);
+      for (int j = 0; j < K; ++j) stage_regs_load<R>(a, rb, cyc(1 + j, nseq), s.r[j]);
     }
   }
   wait_dma_and_barrier();
@@ -350,19 +397,19 @@ __device__ __forceinline__ void stage_prime(const WalkArgs &a, uint32_t rb, Stag
 // Register staging, after walking chunk c (c == J mod K): set J holds chunk
 // c+1; write it to LDS and start loading chunk c+1+K.  The sets loaded after
 // set J stay in flight.
-template <int J, int K>
+template <int J, int K, int R>
 __device__ __forceinline__ void stage_advance_regs(const WalkArgs &a, uint32_t rb, int c,
-                                                   int nseq, Stage<K> &s) {
+                                                   int nseq, Stage<K, R> &s) {
   __syncthreads();  // every wave is done with the buffer
-  stage_regs_store(a, rb, cyc(c + 1, nseq), s.r[J], s.cur);
-  stage_regs_load(a, rb, cyc(c + 1 + K, nseq), s.r[J]);
+  stage_regs_store<R>(a, rb, cyc(c + 1, nseq), s.r[J], s.cur);
+  stage_regs_load<R>(a, rb, cyc(c + 1 + K, nseq), s.r[J]);
   __syncthreads();
 }
 
 // Two buffers or a synchronous copy, after walking chunk c.
-template <int K>
+template <int K, int R>
 __device__ __forceinline__ void stage_advance(const WalkArgs &a, uint32_t rb, int c,
-                                              Stage<K> &s) {
+                                              Stage<K, R> &s) {
   if (a.nchunks == 1) return;
   const int next = cyc(c + 1, a.nchunks);
   if (a.nbuf == 2) {
@@ -380,97 +427,109 @@ __device__ __forceinline__ void stage_advance(const WalkArgs &a, uint32_t rb, in
 
 // Every chunk of the ensemble for the candidates in the tiles; leaves the
 // staging invariant in place for the next round.
-template <int D, int G, int K>
-__device__ __forceinline__ float walk_all(const WalkArgs &a, Stage<K> &s, const char *tile_lane) {
+template <int D, int G, int S, int K, int R>
+__device__ __forceinline__ float walk_all(const WalkArgs &a, Stage<K, R> &s,
+                                          const char *tile_lane, int h) {
   constexpr uint32_t RB = record_bytes(D);
   float m = a.base;
-  if (a.nchunks == 1) return walk_chunk<D, G>(s.cur, a.ntrees, tile_lane, m);
+  if (a.nchunks == 1) return walk_chunk<D, G, S>(s.cur, a.ntrees, tile_lane, h, m);
   if (a.regstage) {
     const int nseq = seq_len<K>(a);
     for (int c = 0; c < nseq; c += K) {
 #pragma unroll
       for (int j = 0; j < K; ++j) {
-        m = walk_chunk<D, G>(s.cur, (int)(chunk_bytes_of(a, RB, c + j) / RB), tile_lane, m);
+        m = walk_chunk<D, G, S>(s.cur, (int)(chunk_bytes_of(a, RB, c + j) / RB), tile_lane, h,
+                                m);
         switch (j) {  // compile-time set index
-          case 0: stage_advance_regs<0, K>(a, RB, c + j, nseq, s); break;
-          case 1: stage_advance_regs<1, K>(a, RB, c + j, nseq, s); break;
-          case 2: if constexpr (K > 2) stage_advance_regs<2, K>(a, RB, c + j, nseq, s); break;
-          default: if constexpr (K > 3) stage_advance_regs<3, K>(a, RB, c + j, nseq, s); break;
+          case 0: stage_advance_regs<0, K, R>(a, RB, c + j, nseq, s); break;
+          case 1: stage_advance_regs<1, K, R>(a, RB, c + j, nseq, s); break;
+          case 2: if constexpr (K > 2) stage_advance_regs<2, K, R>(a, RB, c + j, nseq, s); break;
+          default: if constexpr (K > 3) stage_advance_regs<3, K, R>(a, RB, c + j, nseq, s); break;
         }
       }
     }
   } else {
     for (int c = 0; c < a.nchunks; ++c) {
-      m = walk_chunk<D, G>(s.cur, (int)(chunk_bytes_of(a, RB, c) / RB), tile_lane, m);
+      m = walk_chunk<D, G, S>(s.cur, (int)(chunk_bytes_of(a, RB, c) / RB), tile_lane, h, m);
       stage_advance(a, RB, c, s);
     }
   }
   return m;
 }
 
-template <int D, int G>
-__global__ void __launch_bounds__(kLanes *kMaxWaves) __attribute__((amdgpu_waves_per_eu(1, 1)))
+// With S = 2 a kernel must leave room for two waves per SIMD (256 VGPRs).
+template <int D, int G, int S>
+__global__ void __launch_bounds__(kLanes *kMaxWaves) __attribute__((amdgpu_waves_per_eu(S, S)))
 validity_kernel(WalkArgs a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   constexpr uint32_t RB = record_bytes(D);
+  constexpr int CPW = Geo<S>::kCand;
   const int lane = threadIdx.x & (kLanes - 1);
   const int wave = threadIdx.x / kLanes;
+  const int h = lane / CPW;  // half-wave (0 with S = 1)
+  const int cl = lane % CPW;
   const int W = a.nthreads / kLanes;
-  const size_t tile_bytes = (size_t)a.F * kTileRowBytes;
+  const size_t tile_bytes = (size_t)a.F * Geo<S>::kRowBytes;
   const uint32_t chunk_bytes = (uint32_t)a.chunk_trees * RB;
-  Stage<kValiditySets> st;
+  Stage<kValiditySets, Geo<S>::kStageRegs> st;
   st.cur = smem + W * tile_bytes;
   st.other = st.cur + (a.nbuf == 2 ? chunk_bytes : 0u);
-  char *tile_lane = smem + wave * tile_bytes + 4 * lane;
-  const int64_t ntiles = (a.n + kLanes - 1) / kLanes;
+  char *tile_lane = smem + wave * tile_bytes + 4 * cl;
+  const int64_t ntiles = (a.n + CPW - 1) / CPW;
   stage_prime(a, RB, st);
   RowHead head;
-  if (a.rowpf) row_batch_load(a, ((int64_t)blockIdx.x * W + wave) * kLanes + lane, 0, head.v);
+  if (a.rowpf) row_batch_load(a, ((int64_t)blockIdx.x * W + wave) * CPW + cl, h, head.v);
   for (int64_t tg = blockIdx.x; tg * W < ntiles; tg += gridDim.x) {
-    const int64_t row = (tg * W + wave) * kLanes + lane;
+    const int64_t row = (tg * W + wave) * CPW + cl;
     const bool active = row < a.n;
     if (a.rowpf) {
-      row_commit(a, row, head, tile_lane);
-      row_batch_load(a, ((tg + gridDim.x) * W + wave) * kLanes + lane, 0, head.v);
-    } else if (active) {
-      load_row(a, row, tile_lane);
+      row_commit<S>(a, row, head, h, tile_lane);
+      row_batch_load(a, ((tg + gridDim.x) * W + wave) * CPW + cl, h, head.v);
+    } else if (active && h == 0) {
+      load_row<S>(a, row, tile_lane);
     }
     __syncthreads();
-    const float m = walk_all<D, G>(a, st, tile_lane);
-    if (active) {
+    const float m = walk_all<D, G, S>(a, st, tile_lane, h);
+    if (active && h == 0) {
       __builtin_nontemporal_store((uint8_t)((m > 0.0f) ? 1 : 0), a.valid_out + row);
       if (a.margin_out) __builtin_nontemporal_store(m, a.margin_out + row);
     }
   }
 }
 
-template <int D, int G>
-__global__ void __launch_bounds__(kLanes *kMaxWaves) __attribute__((amdgpu_waves_per_eu(1, 1)))
+template <int D, int G, int S>
+__global__ void __launch_bounds__(kLanes *kMaxWaves) __attribute__((amdgpu_waves_per_eu(S, S)))
 perf_kernel(WalkArgs a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   __shared__ int wave_count[kMaxWaves];
   constexpr uint32_t RB = record_bytes(D);
+  constexpr int CPW = Geo<S>::kCand;
   const int lane = threadIdx.x & (kLanes - 1);
   const int wave = threadIdx.x / kLanes;
-  const int B = a.nthreads;
-  const int W = B / kLanes;
-  const size_t tile_bytes = (size_t)a.F * kTileRowBytes;
+  const int h = lane / CPW;
+  const int cl = lane % CPW;
+  const int NT = a.nthreads;  // mask entries scanned per step
+  const int W = NT / kLanes;
+  const int C = W * CPW;      // candidates walked per round
+  const int cand = wave * CPW + cl;
+  const size_t tile_bytes = (size_t)a.F * Geo<S>::kRowBytes;
   const uint32_t chunk_bytes = (uint32_t)a.chunk_trees * RB;
-  Stage<kPerfSets> st;
+  Stage<kPerfSets, Geo<S>::kStageRegs> st;
   st.cur = smem + W * tile_bytes;
   st.other = st.cur + (a.nbuf == 2 ? chunk_bytes : 0u);
-  int32_t *queue = reinterpret_cast<int32_t *>(st.other + chunk_bytes);  // 2*B entries
-  char *tile_lane = smem + wave * tile_bytes + 4 * lane;
+  int32_t *queue = reinterpret_cast<int32_t *>(st.other + chunk_bytes);  // C + NT entries
+  char *tile_lane = smem + wave * tile_bytes + 4 * cl;
   const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  const int64_t nsteps = (a.n + B - 1) / B;
+  const int64_t nsteps = (a.n + NT - 1) / NT;
   int64_t step = blockIdx.x;
   int qn = 0;  // identical in every thread
   stage_prime(a, RB, st);
-  // Scan the mask B entries at a time until a full tile set is queued (or
-  // the pool is exhausted), then take up to B rows off the queue.
+  // Scan the mask NT entries at a time until C candidates are queued (or the
+  // pool is exhausted), then take up to C rows off the queue.  The queue
+  // never holds more than C - 1 + NT entries.
   auto next_rows = [&]() -> int32_t {
-    while (qn < B && step < nsteps) {
-      const int64_t i = step * B + threadIdx.x;
+    while (qn < C && step < nsteps) {
+      const int64_t i = step * NT + threadIdx.x;
       const bool in = i < a.n;
       const bool v = in && (a.valid_in == nullptr || a.valid_in[i] != 0);
       if (in && !v) __builtin_nontemporal_store(-INFINITY, a.score_out + i);
@@ -488,9 +547,9 @@ perf_kernel(WalkArgs a) {
       step += gridDim.x;
       __syncthreads();
     }
-    const int take = min(qn, B);
-    const int32_t r = (threadIdx.x < take) ? queue[threadIdx.x] : -1;
-    const int rem = qn - take;
+    const int take = min(qn, C);
+    const int32_t r = (cand < take) ? queue[cand] : -1;
+    const int rem = qn - take;  // < NT
     const int32_t carry = (threadIdx.x < rem) ? queue[take + threadIdx.x] : 0;
     __syncthreads();
     if (threadIdx.x < rem) queue[threadIdx.x] = carry;
@@ -500,56 +559,72 @@ perf_kernel(WalkArgs a) {
   };
   RowHead head;
   int32_t row = next_rows();
-  if (a.rowpf) row_batch_load(a, row, 0, head.v);
+  if (a.rowpf) row_batch_load(a, row, h, head.v);
   for (;;) {
     if (__syncthreads_or(row >= 0) == 0) break;
     if (a.rowpf)
-      row_commit(a, row, head, tile_lane);
-    else if (row >= 0)
-      load_row(a, row, tile_lane);
+      row_commit<S>(a, row, head, h, tile_lane);
+    else if (row >= 0 && h == 0)
+      load_row<S>(a, row, tile_lane);
     const int32_t nrow = next_rows();  // ends with a barrier: the tiles are complete
-    if (a.rowpf) row_batch_load(a, nrow, 0, head.v);
-    const float m = walk_all<D, G>(a, st, tile_lane);
-    if (row >= 0) __builtin_nontemporal_store(m, a.score_out + row);
+    if (a.rowpf) row_batch_load(a, nrow, h, head.v);
+    const float m = walk_all<D, G, S>(a, st, tile_lane, h);
+    if (row >= 0 && h == 0) __builtin_nontemporal_store(m, a.score_out + row);
     row = nrow;
   }
 }
 
-// Trees walked concurrently per lane that a depth allows (a chunk must hold
-// at least G whole trees in LDS).
-constexpr bool group_allowed(int d, int g) {
+// Trees walked concurrently per lane that a depth allows.  S = 1: a chunk
+// must hold at least G whole trees.  S = 2: a 24 KiB register-staged chunk
+// must hold the 2G trees of a group.
+constexpr bool group_allowed(int d, int g, int s) {
+  if (s == 2)
+    return d <= 7 ? (g == 4 || g == 8)
+         : d == 8 ? (g == 2 || g == 4)
+         : d == 9 ? (g == 1 || g == 2)
+         : d == 10 ? (g == 1)
+                   : false;
   return d <= 7 ? (g == 8 || g == 16)
        : d <= 9 ? (g == 4 || g == 8)
        : d == 10 ? (g == 2 || g == 4)
                  : (g == 1 || g == 2);
 }
 
-template <int D, int G>
-hipError_t launch_dg(bool perf, const WalkPlan &p, const WalkArgs &a, hipStream_t s) {
-  const void *fn = perf ? reinterpret_cast<const void *>(&perf_kernel<D, G>)
-                        : reinterpret_cast<const void *>(&validity_kernel<D, G>);
+template <int D, int G, int S>
+hipError_t launch_dgs(bool perf, const WalkPlan &p, const WalkArgs &a, hipStream_t s) {
+  const void *fn = perf ? reinterpret_cast<const void *>(&perf_kernel<D, G, S>)
+                        : reinterpret_cast<const void *>(&validity_kernel<D, G, S>);
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
                                      (int)p.lds_bytes);
   if (e != hipSuccess) return e;
   dim3 grid(p.grid), block(p.waves * kLanes);
   if (perf)
-    hipLaunchKernelGGL((perf_kernel<D, G>), grid, block, p.lds_bytes, s, a);
+    hipLaunchKernelGGL((perf_kernel<D, G, S>), grid, block, p.lds_bytes, s, a);
   else
-    hipLaunchKernelGGL((validity_kernel<D, G>), grid, block, p.lds_bytes, s, a);
+    hipLaunchKernelGGL((validity_kernel<D, G, S>), grid, block, p.lds_bytes, s, a);
   return hipGetLastError();
+}
+
+template <int D, int S>
+hipError_t launch_ds(bool perf, const WalkPlan &p, const WalkArgs &a, hipStream_t s) {
+  switch (p.group) {
+    case 1: if constexpr (group_allowed(D, 1, S)) return launch_dgs<D, 1, S>(perf, p, a, s); break;
+    case 2: if constexpr (group_allowed(D, 2, S)) return launch_dgs<D, 2, S>(perf, p, a, s); break;
+    case 4: if constexpr (group_allowed(D, 4, S)) return launch_dgs<D, 4, S>(perf, p, a, s); break;
+    case 8: if constexpr (group_allowed(D, 8, S)) return launch_dgs<D, 8, S>(perf, p, a, s); break;
+    case 16: if constexpr (group_allowed(D, 16, S)) return launch_dgs<D, 16, S>(perf, p, a, s); break;
+    default: break;
+  }
+  return hipErrorInvalidValue;
 }
 
 template <int D>
 hipError_t launch_depth(bool perf, const WalkPlan &p, const WalkArgs &a, hipStream_t s) {
-  switch (p.group) {
-    case 1: if constexpr (group_allowed(D, 1)) return launch_dg<D, 1>(perf, p, a, s); break;
-    case 2: if constexpr (group_allowed(D, 2)) return launch_dg<D, 2>(perf, p, a, s); break;
-    case 4: if constexpr (group_allowed(D, 4)) return launch_dg<D, 4>(perf, p, a, s); break;
-    case 8: if constexpr (group_allowed(D, 8)) return launch_dg<D, 8>(perf, p, a, s); break;
-    case 16: if constexpr (group_allowed(D, 16)) return launch_dg<D, 16>(perf, p, a, s); break;
-    default: break;
+  if (p.split == 2) {
+    if constexpr (D <= 10) return launch_ds<D, 2>(perf, p, a, s);
+    return hipErrorInvalidValue;
   }
-  return hipErrorInvalidValue;
+  return launch_ds<D, 1>(perf, p, a, s);
 }
 
 hipError_t launch_walk(bool perf, const Forest &f, const WalkPlan &p, const WalkArgs &a,
@@ -576,6 +651,10 @@ int env_int(const char *name, int dflt) {
   return (v && *v) ? atoi(v) : dflt;
 }
 
+size_t stage_reg_bytes(const WalkPlan &p) {
+  return (size_t)(6 / p.split) * 16 * kLanes * p.waves;
+}
+
 WalkArgs make_args(const Forest &f, const WalkPlan &p, const float *X, int64_t n, int64_t ld) {
   WalkArgs a{};
   a.X = X;
@@ -588,71 +667,91 @@ WalkArgs make_args(const Forest &f, const WalkPlan &p, const float *X, int64_t n
   a.F = f.num_features;
   a.vec4 = ((reinterpret_cast<uintptr_t>(X) & 15u) == 0 && (ld & 3) == 0) ? 1 : 0;
   a.nbuf = p.nbuf;
-  a.regstage = (p.nbuf == 1 &&
-                (size_t)p.chunk_trees * f.rec_bytes <= (size_t)kStageRegs * 16 * kLanes * p.waves)
-                   ? 1 : 0;
+  a.regstage = (p.nbuf == 1 && (size_t)p.chunk_trees * f.rec_bytes <= stage_reg_bytes(p)) ? 1 : 0;
   a.rowpf = (a.vec4 && (f.num_features % 4) == 0 && f.num_features <= 4 * kRowVecs) ? 1 : 0;
   a.nthreads = p.waves * kLanes;
   a.base = f.base;
   return a;
 }
 
+// One candidate plan: S lanes per candidate, W waves, staging mode (0: one
+// buffer refilled from registers, 1: two buffers, 2: one buffer copied
+// synchronously), G trees per lane.  Returns false if it does not fit.
+bool try_plan(const Forest &f, int64_t n_work, int cu_count, int S, int W, int mode, int G,
+              int want_c, WalkPlan *p) {
+  if (!group_allowed(f.depth, G, S) || W < 1 || W > kMaxWaves) return false;
+  if (S == 2 && mode != 0) return false;  // groups are sized for register staging
+  const size_t rb = f.rec_bytes;
+  const int cpw = kLanes / S;
+  const size_t tile = (size_t)f.num_features * 4 * cpw;
+  // tiles + the perf queue (C + NT entries, C = W * cpw, NT = 64 W)
+  const size_t fixed = (size_t)W * (tile + (size_t)(cpw + kLanes) * sizeof(int32_t));
+  const int nbuf = mode == 1 ? 2 : 1;
+  const int gs = G * S;
+  if (fixed + (size_t)nbuf * gs * rb > kLdsBudget) return false;
+  const size_t room = (kLdsBudget - fixed) / nbuf;
+  const int tpad = (f.num_trees_padded + gs - 1) / gs * gs;
+  int chunk_trees = (int)(room / rb) / gs * gs;
+  WalkPlan q{};
+  q.split = S;
+  q.waves = W;
+  if (mode == 0) {  // the chunk must fit the staging registers
+    const int reg_trees = (int)(stage_reg_bytes(q) / rb) / gs * gs;
+    if (reg_trees < gs) return false;
+    if (chunk_trees > reg_trees) chunk_trees = reg_trees;
+  }
+  if (want_c > 0 && want_c % gs == 0 && want_c <= chunk_trees) chunk_trees = want_c;
+  if (chunk_trees > tpad) chunk_trees = tpad;
+  q.group = G;
+  q.chunk_trees = chunk_trees;
+  q.nbuf = nbuf;
+  q.lds_bytes = fixed + (size_t)nbuf * chunk_trees * rb;
+  int per_cu = (int)(kLdsBudget / q.lds_bytes);
+  if (per_cu < 1) per_cu = 1;
+  if (per_cu > 8) per_cu = 8;
+  const int64_t tiles = (n_work + cpw - 1) / cpw;
+  const int64_t wgs = (tiles + W - 1) / W;
+  int64_t grid = (int64_t)cu_count * per_cu;
+  if (wgs < grid) grid = wgs;
+  if (grid < 1) grid = 1;
+  q.grid = (int)grid;
+  *p = q;
+  return true;
+}
+
 }  // namespace
 
-// LDS of one workgroup = W candidate tiles (F * 256 bytes each, plus the
+// LDS of one workgroup = W candidate tiles (F * 256 / S bytes each, plus the
 // compaction queue share) + nbuf chunk buffers of chunk_trees whole trees
-// (a multiple of G, as large as the LDS allows).  ML2_WALK_GROUP /
-// ML2_WALK_WAVES / ML2_WALK_NBUF / ML2_WALK_CHUNK override the choice
-// (tuning sweeps); out-of-range overrides are ignored.
+// (a multiple of S*G, as large as the LDS allows).  Preference: eight waves
+// (two per SIMD), with one lane per candidate where eight full tiles fit
+// (twice the candidates per pass over the ensemble), else two; then one lane
+// per candidate with four waves in the order register staging, two buffers,
+// synchronous copy; then fewer waves.  Larger G first within each.  ML2_WALK_SPLIT /
+// ML2_WALK_GROUP / ML2_WALK_WAVES / ML2_WALK_NBUF / ML2_WALK_CHUNK override
+// the choice (tuning sweeps); overrides that do not fit are ignored.
 bool plan_walk(const Forest &f, int64_t n_work, int cu_count, WalkPlan *p, const char **why) {
-  const int D = f.depth;
-  const size_t rb = f.rec_bytes;
-  const size_t tile = (size_t)f.num_features * kTileRowBytes;
-  const size_t per_wave = tile + 2 * kLanes * sizeof(int32_t);
+  const int want_s = env_int("ML2_WALK_SPLIT", 0);
   const int want_g = env_int("ML2_WALK_GROUP", 0);
   const int want_w = env_int("ML2_WALK_WAVES", 0);
   const int want_b = env_int("ML2_WALK_NBUF", 0);
   const int want_c = env_int("ML2_WALK_CHUNK", 0);
   const int groups[5] = {16, 8, 4, 2, 1};
-  // Preference: four waves (one per SIMD); then one buffer refilled from
-  // registers, two buffers, one buffer copied synchronously; then larger G.
-  for (int need_w = 4; need_w >= 1; --need_w) {
-    for (int mode = 0; mode < 3; ++mode) {
-      const int nbuf = mode == 1 ? 2 : 1;
-      if (want_b && want_b != nbuf) continue;
-      for (int gi = 0; gi < 5; ++gi) {
-        const int G = groups[gi];
-        if (!group_allowed(D, G)) continue;
-        if (want_g && group_allowed(D, want_g) && G != want_g) continue;
-        int W = need_w;
+  struct Shape { int s, w; };
+  const Shape shapes[] = {{1, 8}, {2, 8}, {1, 4}, {2, 4}, {1, 2}, {1, 1}};
+  for (int pass = 0; pass < 2; ++pass) {  // pass 0 honours the overrides
+    for (const Shape &sh : shapes) {
+      int S = sh.s, W = sh.w;
+      if (pass == 0) {
+        if (want_s && want_s != S) continue;
         if (want_w > 0) W = want_w;
-        if (W > kMaxWaves) continue;
-        if ((size_t)W * per_wave + (size_t)nbuf * G * rb > kLdsBudget) continue;
-        const size_t room = (kLdsBudget - (size_t)W * per_wave) / nbuf;
-        const int tpad = (f.num_trees_padded + G - 1) / G * G;
-        int chunk_trees = (int)(room / rb) / G * G;
-        if (mode == 0) {  // the chunk must fit the staging registers
-          const int reg_trees = (int)((size_t)kStageRegs * 16 * kLanes * W / rb) / G * G;
-          if (reg_trees < G) continue;
-          if (chunk_trees > reg_trees) chunk_trees = reg_trees;
+      }
+      for (int mode = 0; mode < 3; ++mode) {
+        if (pass == 0 && want_b && want_b != (mode == 1 ? 2 : 1)) continue;
+        for (int G : groups) {
+          if (pass == 0 && want_g && group_allowed(f.depth, want_g, S) && G != want_g) continue;
+          if (try_plan(f, n_work, cu_count, S, W, mode, G, pass == 0 ? want_c : 0, p)) return true;
         }
-        if (want_c > 0 && want_c % G == 0 && want_c <= chunk_trees) chunk_trees = want_c;
-        if (chunk_trees > tpad) chunk_trees = tpad;
-        p->waves = W;
-        p->group = G;
-        p->chunk_trees = chunk_trees;
-        p->nbuf = nbuf;
-        p->lds_bytes = (size_t)W * per_wave + (size_t)nbuf * chunk_trees * rb;
-        int per_cu = (int)(kLdsBudget / p->lds_bytes);
-        if (per_cu < 1) per_cu = 1;
-        if (per_cu > 8) per_cu = 8;
-        const int64_t tiles = (n_work + kLanes - 1) / kLanes;
-        const int64_t wgs = (tiles + W - 1) / W;
-        int64_t grid = (int64_t)cu_count * per_cu;
-        if (wgs < grid) grid = wgs;
-        if (grid < 1) grid = 1;
-        p->grid = (int)grid;
-        return true;
       }
     }
   }

@@ -200,6 +200,24 @@ def test_depth_and_width_limits(depth, F, trees):
     check_pipeline(V, P, X, 100)
 
 
+@pytest.mark.parametrize("split,group,waves,nbuf,chunk", [
+    (1, 16, 4, 1, 0), (1, 8, 8, 1, 0), (1, 8, 4, 2, 0), (1, 8, 4, 1, 16),
+    (2, 8, 8, 1, 0), (2, 4, 8, 1, 16), (2, 4, 4, 1, 0), (2, 8, 8, 1, 32),
+])
+def test_walk_plans(monkeypatch, split, group, waves, nbuf, chunk):
+    """Every launch shape of the walks (lanes per candidate, trees per lane,
+    waves, staging mode, chunk size), forced through the tuning overrides."""
+    for key, val in (("SPLIT", split), ("GROUP", group), ("WAVES", waves), ("NBUF", nbuf),
+                     ("CHUNK", chunk)):
+        monkeypatch.setenv(f"ML2_WALK_{key}", str(val))
+    F, K = 40, 20
+    V = gen.perfect_ensemble(31, 1, 70, 7, F, K, 0.5)
+    P = gen.perfect_ensemble(31, 2, 90, 7, F, K, 0.1)
+    X = gen.features(31, 3001, F, K)
+    _note(f"plan S={split} G={group} W={waves} nbuf={nbuf} chunk={chunk}")
+    check_pipeline(V, P, X, 64)
+
+
 def test_perf_without_mask():
     w = gen.WORKLOADS["tiny"]
     check_pipeline(w.validity(), w.perf(), w.features(), 64, perf_mask=False)
