@@ -592,6 +592,9 @@ constexpr bool group_allowed(int d, int g, int s) {
 
 template <int D, int G, int S>
 hipError_t launch_dgs(bool perf, const WalkPlan &p, const WalkArgs &a, hipStream_t s) {
+  // Chunks hold whole groups: every chunk's tree count, including the last
+  // one's, is a multiple of the padding and hence of the group.
+  static_assert(kTreePad % (G * S) == 0, "a walk group must divide the tree padding");
   const void *fn = perf ? reinterpret_cast<const void *>(&perf_kernel<D, G, S>)
                         : reinterpret_cast<const void *>(&validity_kernel<D, G, S>);
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,

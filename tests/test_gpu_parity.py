@@ -200,21 +200,22 @@ def test_depth_and_width_limits(depth, F, trees):
     check_pipeline(V, P, X, 100)
 
 
-@pytest.mark.parametrize("split,group,waves,nbuf,chunk", [
-    (1, 16, 4, 1, 0), (1, 8, 8, 1, 0), (1, 8, 4, 2, 0), (1, 8, 4, 1, 16),
-    (2, 8, 8, 1, 0), (2, 4, 8, 1, 16), (2, 4, 4, 1, 0), (2, 8, 8, 1, 32),
+@pytest.mark.parametrize("split,group,waves,nbuf,chunk,depth", [
+    (1, 16, 4, 1, 0, 7), (1, 8, 8, 1, 0, 7), (1, 8, 4, 2, 0, 7), (1, 8, 4, 1, 16, 7),
+    (2, 8, 8, 1, 0, 7), (2, 4, 8, 1, 16, 7), (2, 4, 4, 1, 0, 7), (2, 8, 8, 1, 32, 7),
+    (2, 4, 8, 1, 16, 6), (2, 2, 8, 1, 0, 8), (2, 1, 8, 1, 0, 9), (2, 1, 8, 1, 0, 10),
 ])
-def test_walk_plans(monkeypatch, split, group, waves, nbuf, chunk):
+def test_walk_plans(monkeypatch, split, group, waves, nbuf, chunk, depth):
     """Every launch shape of the walks (lanes per candidate, trees per lane,
     waves, staging mode, chunk size), forced through the tuning overrides."""
     for key, val in (("SPLIT", split), ("GROUP", group), ("WAVES", waves), ("NBUF", nbuf),
                      ("CHUNK", chunk)):
         monkeypatch.setenv(f"ML2_WALK_{key}", str(val))
     F, K = 40, 20
-    V = gen.perfect_ensemble(31, 1, 70, 7, F, K, 0.5)
-    P = gen.perfect_ensemble(31, 2, 90, 7, F, K, 0.1)
+    V = gen.perfect_ensemble(31, 1, 70, depth, F, K, 0.5)
+    P = gen.perfect_ensemble(31, 2, 90, depth, F, K, 0.1)
     X = gen.features(31, 3001, F, K)
-    _note(f"plan S={split} G={group} W={waves} nbuf={nbuf} chunk={chunk}")
+    _note(f"plan S={split} G={group} W={waves} nbuf={nbuf} chunk={chunk} depth={depth}")
     check_pipeline(V, P, X, 64)
 
 
