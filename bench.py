@@ -32,13 +32,21 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-# VALU lane-instruction ceiling of the chip: 256 CUs x 4 SIMDs x 16 lanes x
-# 2.4 GHz (the fp32 vector peak of 157.3 TFLOP/s counts a packed FMA as 4).
-VALU_LANE_OPS_PER_S = 256 * 4 * 16 * 2.4e9
-# A node visit needs at least two VALU instructions: the comparison
-# x[feature] < threshold and the step to the chosen child.
-VALU_OPS_PER_VISIT = 2
-VISIT_PEAK_PER_S = VALU_LANE_OPS_PER_S / VALU_OPS_PER_VISIT
+# Node-visit ceiling of the chip, from its unit counts and clock (256 CUs,
+# 2.4 GHz).  A visit needs, per lane, two VALU instructions (the comparison
+# x[feature] < threshold and the step to the chosen child) and two LDS reads
+# (the 8-byte node and the 4-byte feature value).
+#   VALU: the fp32 vector peak of 157.3 TFLOP/s is 78.6 T lane-FMAs/s, i.e.
+#         128 lanes per clock per CU -> 39.3 T visits/s.
+#   LDS:  256 bytes per clock per CU (CDNA4 doubled CDNA3's 128; a streaming
+#         ds_read_b128 probe reaches 203 B/clk) -> 157 TB/s / 12 B = 13.1 T
+#         visits/s.
+# The lower one, the LDS ceiling, is the peak.
+VALU_LANE_OPS_PER_S = 256 * 128 * 2.4e9
+VISIT_PEAK_VALU = VALU_LANE_OPS_PER_S / 2
+LDS_BYTES_PER_S = 256 * 256 * 2.4e9
+VISIT_PEAK_LDS = LDS_BYTES_PER_S / 12
+VISIT_PEAK_PER_S = min(VISIT_PEAK_VALU, VISIT_PEAK_LDS)
 METRIC = "candidate configs scored+filtered/sec (validity+perf+top-k); % of HBM peak"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "perf_walk_roofline_traffic.json")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2411_10764_amd", "csrc", "walk_kernels.hip")
@@ -179,6 +187,9 @@ def main() -> int:
     roofline = {
         "bound": "alu",
         "kernel": "perf_kernel (model P walk over accepted candidates)",
+        "peak_derivation": "node visits: LDS 256 B/clk/CU x 256 CU x 2.4 GHz / 12 B per visit "
+                           f"= {VISIT_PEAK_LDS / 1e12:.1f} T/s (VALU: 128 lanes/clk/CU / 2 "
+                           f"instructions per visit = {VISIT_PEAK_VALU / 1e12:.1f} T/s)",
         "achieved": perf_visits_per_s / 1e12,
         "peak": VISIT_PEAK_PER_S / 1e12,
         "unit": "Tvisit/s",

@@ -80,8 +80,9 @@ struct WalkArgs {
 };
 
 // Row `row` of X into the tile of its candidate (dst = tile + 4*candidate),
-// whole, by one lane.  The pool is read once: non-temporal loads keep it from
-// evicting the ensemble from L2.
+// whole, by one lane.  Pool rows are read with plain loads: a line whose
+// 16-byte pieces arrive in separate instructions is fetched from HBM once,
+// where with the non-temporal hint it was measured to be fetched twice.
 template <int S>
 __device__ __forceinline__ void load_row(const WalkArgs &a, int64_t row, char *dst) {
   constexpr uint32_t RW = Geo<S>::kRowBytes;
@@ -89,25 +90,24 @@ __device__ __forceinline__ void load_row(const WalkArgs &a, int64_t row, char *d
   int q = 0;
   if (a.vec4) {
     for (; q + 4 <= a.F; q += 4) {
-      const f32x4 v = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(src + q));
+      const f32x4 v = *reinterpret_cast<const f32x4 *>(src + q);
       *reinterpret_cast<float *>(dst + (q + 0) * RW) = v.x;
       *reinterpret_cast<float *>(dst + (q + 1) * RW) = v.y;
       *reinterpret_cast<float *>(dst + (q + 2) * RW) = v.z;
       *reinterpret_cast<float *>(dst + (q + 3) * RW) = v.w;
     }
   }
-  for (; q < a.F; ++q)
-    *reinterpret_cast<float *>(dst + q * RW) = __builtin_nontemporal_load(src + q);
+  for (; q < a.F; ++q) *reinterpret_cast<float *>(dst + q * RW) = src[q];
 }
 
 // Rows of pools with at most kRowVecs*4 features and 16-byte aligned rows
 // load in batches of 8 vectors, one 128-byte line per row and batch: a wave
-// then never has two requests for the same line in flight, which would
-// fetch the line again and evict the ensemble from L2.  With S lanes per
-// candidate, lane half h loads batches h, h+S, ...  The first batch of the
-// next round's rows is fetched while the current round is walked.  Loads are
-// unconditional (a missing row reads row 0, a short row repeats its last
-// vector), so the compiler knows how many are in flight.
+// then never has requests for many lines of one row in flight at once, which
+// was measured to fetch lines again and evict the ensemble from L2.  With S
+// lanes per candidate, lane half h loads batches h, h+S, ...  The first batch
+// of the next round's rows is fetched while the current round is walked.
+// Loads are unconditional (a missing row reads row 0, a short row repeats its
+// last vector), so the compiler knows how many are in flight.
 constexpr int kRowVecs = 32;
 constexpr int kRowBatch = 8;
 
@@ -126,7 +126,7 @@ __device__ __forceinline__ void row_batch_load(const WalkArgs &a, int64_t row, i
   const int last = a.F / 4 - 1;
 #pragma unroll
   for (int k = 0; k < kRowBatch; ++k)
-    v[k] = __builtin_nontemporal_load(src + min(b * kRowBatch + k, last));
+    v[k] = src[min(b * kRowBatch + k, last)];
 }
 
 template <int S>
