@@ -166,13 +166,29 @@ class Workload:
     seed: int
     base_v: float = 0.0          # validity margin bias (float32 value)
     calib_quantile: float | None = None  # invalid fraction base_v was fixed for
+    # Second level (model A) and the paper's feature split: with
+    # visible_only, V and P split on the K knob columns only (their
+    # num_features is K) and A, over all F columns, re-ranks the k held
+    # configurations and keeps `keep`.
+    a_trees: int = 0
+    a_depth: int = 0
+    keep: int = 0
+    visible_only: bool = False
+
+    def _vp_features(self) -> int:
+        return self.K if self.visible_only else self.F
 
     def validity(self) -> Ensemble:
         return perfect_ensemble(self.seed, STREAM_VALIDITY, self.v_trees, self.v_depth,
-                                self.F, self.K, 0.5, self.base_v)
+                                self._vp_features(), self.K, 0.5, self.base_v)
 
     def perf(self) -> Ensemble:
         return perfect_ensemble(self.seed, STREAM_PERF, self.p_trees, self.p_depth,
+                                self._vp_features(), self.K, 0.1, 0.0)
+
+    def second_level(self) -> Ensemble:
+        assert self.a_trees > 0, f"workload {self.name} has no second-level model"
+        return perfect_ensemble(self.seed, STREAM_SECOND_LEVEL, self.a_trees, self.a_depth,
                                 self.F, self.K, 0.1, 0.0)
 
     def features(self, rows=None, **kw) -> np.ndarray:
@@ -194,5 +210,11 @@ WORKLOADS = {
     "roofline": Workload("roofline", 16777216, 128, 64, 300, 6, 1000, 8, 1024, 4),
     "skewed": Workload("skewed", 8388608, 64, 32, 200, 6, 800, 10, 256, 5,
                        _BASE_V_SKEWED, 0.9),
+    # The explorer as the paper runs it (Section 2): V and P on the visible
+    # (knob) columns, A (300 rounds as in Table 3, depth 12 = the deepest
+    # perfect layout; Table 3's 14 needs the ragged layout) on visible +
+    # hidden columns; k = (alpha+1)N = 1024 held, N = 512 kept (alpha = 1).
+    "explorer": Workload("explorer", 16777216, 128, 64, 300, 6, 1000, 8, 1024, 6,
+                         a_trees=300, a_depth=12, keep=512, visible_only=True),
 }
 CALIBRATION_ROWS = 65536

@@ -51,7 +51,7 @@ typedef enum {
 /* Library limits (checked at load / call time, ML2_ERR_UNSUPPORTED beyond). */
 #define ML2_MAX_DEPTH 12        /* longest root-to-leaf path, in splits */
 #define ML2_MAX_FEATURES 256    /* num_features of an ensemble */
-#define ML2_MAX_TOPK 16384      /* k of ml2_filter_topk */
+#define ML2_MAX_TOPK 16384      /* k of ml2_filter_topk; m and keep of ml2_rerank */
 
 typedef struct ml2_ensemble ml2_ensemble; /* opaque; immutable after load */
 
@@ -158,6 +158,32 @@ ml2_status ml2_topk_workspace_bytes(int64_t n, int32_t k, size_t *bytes);
 ml2_status ml2_filter_topk(const uint8_t *valid, const float *scores, int64_t n, int32_t k,
                            int32_t *topk_idx, float *topk_score, int32_t *num_selected,
                            void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Second-level selection (model A, Section 2 "Hidden Feature Extractor & ML
+ * Model A"): of the (alpha+1)*N configurations the explorer holds, model A,
+ * which sees the hidden features as well as the visible ones, picks the N
+ * expected to perform best.  For i in [0, m):
+ *   row_scores[i] = fold of a over row rows[i] of X   if 0 <= rows[i] < n
+ *                 = -infinity                          otherwise (skipped)
+ * The listed rows in range are ordered by row_scores descending, then pool
+ * row ascending (-0.0 and +0.0 are equal; a row listed twice is taken twice).
+ * Writes
+ *   out_idx[j], out_score[j]  for j < min(keep, #in range): pool row and its
+ *                             score (a zero score is written as +0.0)
+ *   out_idx[j] = -1, out_score[j] = -inf for the remaining slots
+ *   *num_selected = min(keep, #in range)        (int32, device)
+ * X: float32 [n][ld] device, as in ml2_score_validity (a's features may be
+ * more columns than those V and P use); rows: int32 [m] device, e.g. the
+ * topk_idx of ml2_filter_topk (its -1 padding is skipped); row_scores:
+ * float32 [m] device; out_idx: int32 [keep], out_score: float32 [keep],
+ * num_selected: int32 [1], all device.  No workspace.
+ * Errors: INVALID_ARG (NULL pointers, m < 0, keep < 0, n out of range,
+ * ld < F, misaligned X), UNSUPPORTED (m or keep > ML2_MAX_TOPK), HIP.
+ */
+ml2_status ml2_rerank(const ml2_ensemble *a, const float *X, int64_t n, int64_t ld,
+                      const int32_t *rows, int32_t m, int32_t keep, float *row_scores,
+                      int32_t *out_idx, float *out_score, int32_t *num_selected, void *stream);
 
 /* Thread-local description of the last non-OK status on this thread. */
 const char *ml2_last_error(void);

@@ -68,6 +68,9 @@ def _load():
         lib.ml2o_perf.argtypes = [P, P, ctypes.c_int64, ctypes.c_int64, P, P, ctypes.c_int32]
         lib.ml2o_topk.restype = ctypes.c_int64
         lib.ml2o_topk.argtypes = [P, P, ctypes.c_int64, ctypes.c_int64, P, P]
+        lib.ml2o_rerank.restype = ctypes.c_int64
+        lib.ml2o_rerank.argtypes = [P, P, ctypes.c_int64, ctypes.c_int64, P, ctypes.c_int64,
+                                    ctypes.c_int64, P, P, P]
         _lib = lib
     return _lib
 
@@ -170,6 +173,26 @@ def topk(valid, score, k: int):
     if sel < 0:
         raise MemoryError("oracle top-k allocation failed")
     return idx, out, int(sel)
+
+
+def rerank(a_ens, X, rows, keep: int):
+    """Model A's second level: (row_scores f32 [m], idx i32 [keep],
+    score f32 [keep], num_selected) over the pool rows listed in `rows`
+    (entries outside [0, n) are skipped), by (score desc, row asc)."""
+    e = _as_oracle(a_ens)
+    X = np.ascontiguousarray(X, np.float32)
+    n, ld = (X.shape[0], X.shape[1]) if X.ndim == 2 else (0, 1)
+    assert n == 0 or ld >= e.num_features
+    rows = np.ascontiguousarray(rows, np.int32)
+    m = rows.shape[0]
+    row_scores = np.empty(max(m, 1), np.float32)
+    idx = np.empty(max(keep, 1), np.int32)
+    out = np.empty(max(keep, 1), np.float32)
+    sel = _load().ml2o_rerank(e.ptr, X.ctypes.data if n else None, n, ld, rows.ctypes.data, m,
+                              keep, row_scores.ctypes.data, idx.ctypes.data, out.ctypes.data)
+    if sel < 0:
+        raise MemoryError("oracle re-rank allocation failed")
+    return row_scores[:m], idx[:keep], out[:keep], int(sel)
 
 
 def pipeline(v_ens, p_ens, X, k: int, threads: int = 1):

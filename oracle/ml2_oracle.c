@@ -14,7 +14,10 @@
  *     accepts, until (alpha+1)*N are held ("ML Model V", "Hidden Feature
  *     Extractor & ML Model A").  On a fixed pool this is the top-k by P among
  *     the V-accepted candidates with k = (alpha+1)*N;
- *   - both models are XGBoost tree ensembles (Section 3 "Experimental Setup";
+ *   - model A re-ranks the configurations held, using the hidden features as
+ *     well, and keeps the N it predicts best ("Hidden Feature Extractor & ML
+ *     Model A"): ml2o_rerank;
+ *   - the models are XGBoost tree ensembles (Section 3 "Experimental Setup";
  *     Table 3): V uses the binary hinge objective, whose class decision is 1
  *     exactly when the raw margin is positive; P uses squared-error
  *     regression, whose prediction is the raw margin.
@@ -196,6 +199,52 @@ int64_t ml2o_topk(const uint8_t *valid, const float *score, int64_t n, int64_t k
     if (j < sel) {
       idx[j] = (int32_t)all[j].i;
       out_score[j] = all[j].s;
+    } else {
+      idx[j] = -1;
+      out_score[j] = -INFINITY;
+    }
+  }
+  free(all);
+  return sel;
+}
+
+/*
+ * Second level, model A (Section 2, "Hidden Feature Extractor & ML Model A"):
+ * of the configurations the explorer holds, the ones model A -- which also
+ * sees the hidden features -- predicts to perform best are kept.
+ * rows[0..m) list pool rows of X (n rows, stride ld).  Entry i with
+ * 0 <= rows[i] < n gets row_scores[i] = margin under a; any other entry gets
+ * -inf and is skipped.  The scored entries are ordered by (score desc, row
+ * asc), a row listed twice counting twice, and the first min(keep, #scored)
+ * are written (a zero score as +0.0, since -0 == +0 in the order); the other
+ * keep slots get -1 / -inf.  Returns the number written, -1 on allocation
+ * failure.
+ */
+int64_t ml2o_rerank(const ml2o_ensemble *a, const float *X, int64_t n, int64_t ld,
+                    const int32_t *rows, int64_t m, int64_t keep, float *row_scores,
+                    int32_t *idx, float *out_score) {
+  pair *all = (pair *)malloc((size_t)(m > 0 ? m : 1) * sizeof(pair));
+  if (!all) return -1;
+  int64_t c = 0;
+  for (int64_t i = 0; i < m; ++i) {
+    const int32_t r = rows[i];
+    if (r < 0 || (int64_t)r >= n) {
+      row_scores[i] = -INFINITY;
+      continue;
+    }
+    const float s = ml2o_margin(a, X + (int64_t)r * ld);
+    row_scores[i] = s;
+    if (isnan(s)) continue;
+    all[c].s = s;
+    all[c].i = r;
+    ++c;
+  }
+  qsort(all, (size_t)c, sizeof(pair), by_score_then_index);
+  const int64_t sel = c < keep ? c : keep;
+  for (int64_t j = 0; j < keep; ++j) {
+    if (j < sel) {
+      idx[j] = (int32_t)all[j].i;
+      out_score[j] = (all[j].s == 0.0f) ? 0.0f : all[j].s;
     } else {
       idx[j] = -1;
       out_score[j] = -INFINITY;

@@ -351,4 +351,40 @@ ml2_status ml2_filter_topk(const uint8_t *valid, const float *scores, int64_t n,
   return ML2_OK;
 }
 
+ml2_status ml2_rerank(const ml2_ensemble *a, const float *X, int64_t n, int64_t ld,
+                      const int32_t *rows, int32_t m, int32_t keep, float *row_scores,
+                      int32_t *out_idx, float *out_score, int32_t *num_selected, void *stream) {
+  int dev = 0;
+  ml2_status st = check_stream_args(a, X, n, ld, X, "ml2_rerank", &dev);
+  if (st != ML2_OK) return st;
+  if (m < 0) return fail(ML2_ERR_INVALID_ARG, "ml2_rerank: m = %d < 0", m);
+  if (keep < 0) return fail(ML2_ERR_INVALID_ARG, "ml2_rerank: keep = %d < 0", keep);
+  if (m > ML2_MAX_TOPK || keep > ML2_MAX_TOPK)
+    return fail(ML2_ERR_UNSUPPORTED, "ml2_rerank: m = %d or keep = %d > %d", m, keep,
+                ML2_MAX_TOPK);
+  if (!num_selected) return fail(ML2_ERR_INVALID_ARG, "ml2_rerank: num_selected is NULL");
+  if (m > 0 && (!rows || !row_scores))
+    return fail(ML2_ERR_INVALID_ARG, "ml2_rerank: NULL rows or row_scores");
+  if (keep > 0 && (!out_idx || !out_score))
+    return fail(ML2_ERR_INVALID_ARG, "ml2_rerank: NULL output array");
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (m > 0 && n > 0) {
+    ml2::WalkPlan p;
+    const char *why = nullptr;
+    if (!ml2::plan_walk(a->f, m, cu_count(dev), &p, &why))
+      return fail(ML2_ERR_UNSUPPORTED, "ml2_rerank: %s", why);
+    hipError_t e = ml2::launch_rows(a->f, p, X, n, ld, rows, m, row_scores, s);
+    if (e != hipSuccess) return hip_fail(e, "rerank walk launch");
+  }
+  if (m > 0 && n == 0) {  // no listed row is in range (and X may be NULL)
+    hipError_t e = hipMemsetD32Async(reinterpret_cast<hipDeviceptr_t>(row_scores), 0xFF800000u,
+                                     (size_t)m, s);
+    if (e != hipSuccess) return hip_fail(e, "rerank score fill");
+  }
+  hipError_t e = ml2::launch_rerank_select(rows, row_scores, m, n, keep, out_idx, out_score,
+                                           num_selected, s);
+  if (e != hipSuccess) return hip_fail(e, "rerank select launch");
+  return ML2_OK;
+}
+
 }  // extern "C"

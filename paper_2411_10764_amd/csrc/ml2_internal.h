@@ -62,9 +62,19 @@ hipError_t launch_validity(const Forest &f, const WalkPlan &p, const float *X, i
 hipError_t launch_perf(const Forest &f, const WalkPlan &p, const float *X, int64_t n,
                        int64_t ld, const uint8_t *valid, float *score_out, hipStream_t s);
 
+// Perf walk over a list of pool rows: score_out[i] = margin of row rows[i],
+// or -inf where rows[i] lies outside [0, n).
+hipError_t launch_rows(const Forest &f, const WalkPlan &p, const float *X, int64_t n, int64_t ld,
+                       const int32_t *rows, int32_t m, float *score_out, hipStream_t s);
+
 size_t topk_workspace_bytes(int64_t n, int32_t k);
 hipError_t launch_topk(const uint8_t *valid, const float *scores, int64_t n, int32_t k,
                        int32_t *idx, float *score, int32_t *num, void *ws, int cu_count,
                        hipStream_t s);
+
+// The `keep` best of m listed rows by (score desc, pool row asc); m <= ML2_MAX_TOPK.
+hipError_t launch_rerank_select(const int32_t *rows, const float *scores, int32_t m, int64_t n,
+                                int32_t keep, int32_t *idx, float *score, int32_t *num,
+                                hipStream_t s);
 
 }  // namespace ml2

@@ -228,6 +228,73 @@ __global__ void __launch_bounds__(kSortThreads) topk_sort(const float *scores, T
   if (threadIdx.x == 0) *num = cnt;
 }
 
+// Float32 of an order-preserving key's high word (inverse of make_key's map;
+// a zero comes back as +0.0).
+__device__ __forceinline__ float key_score(unsigned long long key) {
+  const uint32_t ord = (uint32_t)(key >> 32);
+  const uint32_t b = (ord & 0x80000000u) ? (ord & 0x7FFFFFFFu) : ~ord;
+  return __uint_as_float(b);
+}
+
+// Second-level selection (model A): one workgroup sorts the keys of the m
+// listed rows, (ord(score) << 32) | (0xFFFFFFFF - row), and writes the best
+// `keep`.  Rows outside [0, n) and NaN scores are left out (key 0, below
+// every included key: a zero high word is the ord of a negative NaN).
+__global__ void __launch_bounds__(kSortThreads) rerank_select(const int32_t *rows,
+                                                              const float *scores, int32_t m,
+                                                              int64_t n, int32_t keep,
+                                                              int32_t *idx, float *out,
+                                                              int32_t *num) {
+  extern __shared__ unsigned long long keys[];
+  __shared__ int included_s;
+  if (threadIdx.x == 0) included_s = 0;
+  int size = 1;
+  while (size < m) size <<= 1;
+  __syncthreads();
+  int mine = 0;
+  for (int j = threadIdx.x; j < size; j += blockDim.x) {
+    unsigned long long key = 0ull;
+    if (j < m) {
+      const int32_t r = rows[j];
+      const float sc = scores[j];
+      if (r >= 0 && r < n && !isnan(sc)) {
+        key = make_key(sc, r);
+        ++mine;
+      }
+    }
+    keys[j] = key;
+  }
+  if (mine) atomicAdd(&included_s, mine);
+  __syncthreads();
+  for (int len = 2; len <= size; len <<= 1) {
+    for (int stride = len >> 1; stride > 0; stride >>= 1) {
+      for (int j = threadIdx.x; j < size; j += blockDim.x) {
+        const int p = j ^ stride;
+        if (p > j) {
+          const unsigned long long a = keys[j], b = keys[p];
+          const bool desc = (j & len) == 0;
+          if (desc ? (a < b) : (a > b)) {
+            keys[j] = b;
+            keys[p] = a;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  const int cnt = min(included_s, keep);
+  for (int j = threadIdx.x; j < keep; j += blockDim.x) {
+    if (j < cnt) {
+      idx[j] = (int32_t)(0xFFFFFFFFu - (uint32_t)(keys[j] & 0xFFFFFFFFull));
+      out[j] = key_score(keys[j]);
+    } else {
+      idx[j] = -1;
+      out[j] = -INFINITY;
+    }
+  }
+  if (threadIdx.x == 0) *num = cnt;
+}
+
 }  // namespace
 
 size_t topk_workspace_bytes(int64_t n, int32_t k) {
@@ -269,6 +336,20 @@ hipError_t launch_topk(const uint8_t *valid, const float *scores, int64_t n, int
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(topk_sort, dim3(1), dim3(kSortThreads), lds, s, scores, st, cand, idx,
                      score, num);
+  return hipGetLastError();
+}
+
+hipError_t launch_rerank_select(const int32_t *rows, const float *scores, int32_t m, int64_t n,
+                                int32_t keep, int32_t *idx, float *score, int32_t *num,
+                                hipStream_t s) {
+  int size = 1;
+  while (size < m) size <<= 1;
+  const size_t lds = (size_t)size * sizeof(unsigned long long);
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&rerank_select),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(rerank_select, dim3(1), dim3(kSortThreads), lds, s, rows, scores, m, n, keep,
+                     idx, score, num);
   return hipGetLastError();
 }
 

@@ -56,7 +56,8 @@ struct Geo {
 
 struct WalkArgs {
   const float *X;
-  int64_t n;
+  int64_t n;            // entries walked: pool rows, or list positions
+  int64_t n_pool;       // rows of X
   int64_t ld;
   const char *trees;
   int32_t ntrees;       // padded tree count
@@ -76,8 +77,16 @@ struct WalkArgs {
   uint8_t *valid_out;   // validity
   float *margin_out;
   const uint8_t *valid_in;  // perf
-  float *score_out;
+  const int32_t *rows_in;   // perf over a row list: entry i is pool row rows_in[i]
+  float *score_out;         // perf: one score per entry
 };
+
+// Pool row of entry `pos` (-1 for none).  List entries outside [0, n_pool)
+// are never queued.
+__device__ __forceinline__ int64_t pool_row(const WalkArgs &a, int32_t pos) {
+  if (pos < 0) return -1;
+  return a.rows_in ? (int64_t)a.rows_in[pos] : (int64_t)pos;
+}
 
 // Row `row` of X into the tile of its candidate (dst = tile + 4*candidate),
 // whole, by one lane.  Pool rows are read with plain loads: a line whose
@@ -116,7 +125,7 @@ struct RowHead {
 };
 
 __device__ __forceinline__ const f32x4 *row_src(const WalkArgs &a, int64_t row) {
-  const int64_t rr = (row >= 0 && row < a.n) ? row : 0;
+  const int64_t rr = (row >= 0 && row < a.n_pool) ? row : 0;
   return reinterpret_cast<const f32x4 *>(a.X + rr * a.ld);
 }
 
@@ -531,7 +540,13 @@ perf_kernel(WalkArgs a) {
     while (qn < C && step < nsteps) {
       const int64_t i = step * NT + threadIdx.x;
       const bool in = i < a.n;
-      const bool v = in && (a.valid_in == nullptr || a.valid_in[i] != 0);
+      bool v = in;
+      if (in && a.rows_in) {
+        const int32_t r = a.rows_in[i];
+        v = r >= 0 && r < a.n_pool;
+      } else if (in && a.valid_in) {
+        v = a.valid_in[i] != 0;
+      }
       if (in && !v) __builtin_nontemporal_store(-INFINITY, a.score_out + i);
       const uint64_t bal = __ballot(v);
       if (lane == 0) wave_count[wave] = __popcll(bal);
@@ -557,19 +572,23 @@ perf_kernel(WalkArgs a) {
     __syncthreads();
     return r;
   };
+  // `pos` is an entry (a pool row, or a list position), `row` its pool row.
   RowHead head;
-  int32_t row = next_rows();
+  int32_t pos = next_rows();
+  int64_t row = pool_row(a, pos);
   if (a.rowpf) row_batch_load(a, row, h, head.v);
   for (;;) {
-    if (__syncthreads_or(row >= 0) == 0) break;
+    if (__syncthreads_or(pos >= 0) == 0) break;
     if (a.rowpf)
       row_commit<S>(a, row, head, h, tile_lane);
     else if (row >= 0 && h == 0)
       load_row<S>(a, row, tile_lane);
-    const int32_t nrow = next_rows();  // ends with a barrier: the tiles are complete
+    const int32_t npos = next_rows();  // ends with a barrier: the tiles are complete
+    const int64_t nrow = pool_row(a, npos);
     if (a.rowpf) row_batch_load(a, nrow, h, head.v);
     const float m = walk_all<D, G, S>(a, st, tile_lane, h);
-    if (row >= 0 && h == 0) __builtin_nontemporal_store(m, a.score_out + row);
+    if (pos >= 0 && h == 0) __builtin_nontemporal_store(m, a.score_out + pos);
+    pos = npos;
     row = nrow;
   }
 }
@@ -662,6 +681,7 @@ WalkArgs make_args(const Forest &f, const WalkPlan &p, const float *X, int64_t n
   WalkArgs a{};
   a.X = X;
   a.n = n;
+  a.n_pool = n;
   a.ld = ld;
   a.trees = static_cast<const char *>(f.d_trees);
   a.ntrees = f.num_trees_padded;
@@ -774,6 +794,15 @@ hipError_t launch_perf(const Forest &f, const WalkPlan &p, const float *X, int64
                        int64_t ld, const uint8_t *valid, float *score_out, hipStream_t s) {
   WalkArgs a = make_args(f, p, X, n, ld);
   a.valid_in = valid;
+  a.score_out = score_out;
+  return launch_walk(true, f, p, a, s);
+}
+
+hipError_t launch_rows(const Forest &f, const WalkPlan &p, const float *X, int64_t n, int64_t ld,
+                       const int32_t *rows, int32_t m, float *score_out, hipStream_t s) {
+  WalkArgs a = make_args(f, p, X, m, ld);
+  a.n_pool = n;
+  a.rows_in = rows;
   a.score_out = score_out;
   return launch_walk(true, f, p, a, s);
 }

@@ -28,7 +28,8 @@ ML2_MAX_TOPK = 16384
 EXPORTED = (
     "ml2_load_ensemble", "ml2_free_ensemble", "ml2_ensemble_num_features",
     "ml2_ensemble_num_trees", "ml2_ensemble_depth", "ml2_score_validity",
-    "ml2_score_perf", "ml2_topk_workspace_bytes", "ml2_filter_topk", "ml2_last_error",
+    "ml2_score_perf", "ml2_topk_workspace_bytes", "ml2_filter_topk", "ml2_rerank",
+    "ml2_last_error",
 )
 
 
@@ -79,6 +80,8 @@ def lib():
         L.ml2_topk_workspace_bytes.argtypes = [I64, I32, ctypes.POINTER(SZ)]
         L.ml2_filter_topk.restype = I32
         L.ml2_filter_topk.argtypes = [P, P, I64, I32, P, P, P, P, SZ, P]
+        L.ml2_rerank.restype = I32
+        L.ml2_rerank.argtypes = [P, P, I64, I64, P, I32, I32, P, P, P, P, P]
         L.ml2_last_error.restype = ctypes.c_char_p
         L.ml2_last_error.argtypes = []
         _lib = L
@@ -206,6 +209,16 @@ def ml2_filter_topk(valid, scores, k: int, topk_idx, topk_score, num_selected, w
     _check(lib().ml2_filter_topk(_ptr(valid), _ptr(scores), n, k, _ptr(topk_idx),
                                  _ptr(topk_score), _ptr(num_selected), _ptr(workspace),
                                  workspace_bytes, _stream(stream)))
+
+
+def ml2_rerank(a: Ensemble, X, rows, keep: int, row_scores, out_idx, out_score, num_selected,
+               m: int | None = None, stream=None) -> None:
+    xp, n, ld = _rows(X)
+    if m is None:
+        m = rows.shape[0]
+    _check(lib().ml2_rerank(a.handle, xp, n, ld, _ptr(rows), m, keep, _ptr(row_scores),
+                            _ptr(out_idx), _ptr(out_score), _ptr(num_selected),
+                            _stream(stream)))
 
 
 class Pipeline:

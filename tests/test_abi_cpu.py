@@ -172,3 +172,10 @@ def test_filter_topk_argument_errors():
         assert st == ml2.ML2_ERR_INVALID_ARG, c
     st = L.ml2_filter_topk(None, P, 100, ml2.ML2_MAX_TOPK + 1, P, P, P, P, 1 << 30, None)
     assert st == ml2.ML2_ERR_UNSUPPORTED
+
+
+def test_rerank_null_ensemble():
+    L = ml2.lib()
+    P = 1 << 20  # never dereferenced: the NULL ensemble fails validation first
+    assert L.ml2_rerank(None, P, 10, 4, P, 5, 3, P, P, P, P, None) == ml2.ML2_ERR_INVALID_ARG
+    assert b"NULL" in L.ml2_last_error()
