@@ -91,13 +91,17 @@ def cpu_baseline(w, rows: int):
     threads = gen.default_threads()
     X = w.features(rows=np.arange(rows, dtype=np.int64))
     V, P = oracle.OracleEnsemble(w.validity()), oracle.OracleEnsemble(w.perf())
+    A = oracle.OracleEnsemble(w.second_level()) if w.a_trees else None
     t0 = time.perf_counter()
-    oracle.pipeline(V, P, X, w.k, threads=threads)
+    out = oracle.pipeline(V, P, X, w.k, threads=threads)
+    if A is not None:
+        oracle.rerank(A, X, out["idx"], w.keep)
     dt = time.perf_counter() - t0
+    steps = f"validity -> masked perf -> top-{w.k}" + (f" -> model A keeps {w.keep}" if A else "")
     return {"value": rows / dt, "unit": "candidates/s", "cores": threads, "kind": "oracle",
             "sample": f"first {rows} candidates of the {w.name} pool ({w.F} features), "
-                      f"validity -> masked perf -> top-{w.k}, {dt:.2f} s wall on {threads} "
-                      f"threads ({os.cpu_count()} visible cpus)"}
+                      f"{steps}, {dt:.2f} s wall on {threads} threads "
+                      f"({os.cpu_count()} visible cpus)"}
 
 
 def main() -> int:
@@ -144,41 +148,65 @@ def main() -> int:
     v = ml2.ml2_load_ensemble(w.validity())
     p = ml2.ml2_load_ensemble(w.perf())
     pipe = ml2.Pipeline(v, p, w.n, w.k, device=dev)
+    second = w.a_trees > 0
+    if second:  # model A re-ranks the k held configurations and keeps w.keep
+        a = ml2.ml2_load_ensemble(w.second_level())
+        a_scores = torch.empty(w.k, dtype=torch.float32, device=dev)
+        a_idx = torch.empty(w.keep, dtype=torch.int32, device=dev)
+        a_top = torch.empty(w.keep, dtype=torch.float32, device=dev)
+        a_num = torch.empty(1, dtype=torch.int32, device=dev)
     stream = torch.cuda.current_stream()
 
+    def step(e=None):
+        if e is not None:
+            e[0].record(stream)
+        ml2.ml2_score_validity(v, X, pipe.valid, None, stream)
+        if e is not None:
+            e[1].record(stream)
+        ml2.ml2_score_perf(p, X, pipe.valid, pipe.score, stream)
+        if e is not None:
+            e[2].record(stream)
+        ml2.ml2_filter_topk(pipe.valid, pipe.score, w.k, pipe.idx, pipe.top, pipe.num, pipe.ws,
+                            pipe.ws_bytes, w.n, stream)
+        if e is not None:
+            e[3].record(stream)
+        if second:
+            ml2.ml2_rerank(a, X, pipe.idx, w.keep, a_scores, a_idx, a_top, a_num, m=w.k,
+                           stream=stream)
+        if e is not None:
+            e[4].record(stream)
+
     for _ in range(args.warmup):
-        pipe.run(X)
+        step()
     torch.cuda.synchronize()
     _log(f"warmup done ({args.warmup} steps)")
 
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     start = time.perf_counter()
     for s in range(args.steps):
-        e = ev[s]
-        e[0].record(stream)
-        ml2.ml2_score_validity(v, X, pipe.valid, None, stream)
-        e[1].record(stream)
-        ml2.ml2_score_perf(p, X, pipe.valid, pipe.score, stream)
-        e[2].record(stream)
-        ml2.ml2_filter_topk(pipe.valid, pipe.score, w.k, pipe.idx, pipe.top, pipe.num, pipe.ws,
-                            pipe.ws_bytes, w.n, stream)
-        e[3].record(stream)
+        step(ev[s])
     torch.cuda.synchronize()
     wall = time.perf_counter() - start
     t_val = np.mean([e[0].elapsed_time(e[1]) for e in ev])
     t_perf = np.mean([e[1].elapsed_time(e[2]) for e in ev])
     t_topk = np.mean([e[2].elapsed_time(e[3]) for e in ev])
-    t_step = np.mean([e[0].elapsed_time(e[3]) for e in ev])
+    t_rerank = np.mean([e[3].elapsed_time(e[4]) for e in ev])
+    t_step = np.mean([e[0].elapsed_time(e[4]) for e in ev])
     ms_per_step = 1000.0 * wall / args.steps
     valid = pipe.valid.cpu().numpy()
     n_valid = int(valid.sum())
     num = int(pipe.num.item())
     _log(f"step {ms_per_step:.3f} ms (events {t_step:.3f}): validity {t_val:.3f} ms, "
-         f"perf {t_perf:.3f} ms, top-k {t_topk:.3f} ms; valid {n_valid}/{w.n}, selected {num}")
+         f"perf {t_perf:.3f} ms, top-k {t_topk:.3f} ms"
+         + (f", re-rank {t_rerank:.3f} ms (kept {int(a_num.item())})" if second else "")
+         + f"; valid {n_valid}/{w.n}, selected {num}")
 
     value = w.n / (ms_per_step / 1000.0)
-    alg_bytes = 4.0 * w.F * w.n + w.n + 8.0 * w.k
+    f_vp = w.K if w.visible_only else w.F
+    alg_bytes = 4.0 * f_vp * w.n + w.n + 8.0 * w.k
+    if second:
+        alg_bytes += 4.0 * w.F * w.k + 8.0 * w.keep
     visits_v = w.n * w.v_trees * w.v_depth
     visits_p = n_valid * w.p_trees * w.p_depth
     sha = _kernel_sha()
@@ -215,9 +243,13 @@ def main() -> int:
                    "knob_features": w.K, "validity": f"{w.v_trees} trees x depth {w.v_depth}",
                    "perf": f"{w.p_trees} trees x depth {w.p_depth}", "k": w.k,
                    "seed": w.seed, "invalid_fraction": 1 - n_valid / w.n},
+        **({"second_level": {"model_a": f"{w.a_trees} trees x depth {w.a_depth} over {w.F} "
+                                        f"features", "keep": w.keep,
+                             "validity_perf_features": f_vp}} if second else {}),
         "roofline": roofline,
         "hbm_frac": roofline["hbm"]["frac"],
-        "kernel_ms": {"validity": t_val, "perf": t_perf, "topk": t_topk},
+        "kernel_ms": {"validity": t_val, "perf": t_perf, "topk": t_topk,
+                      **({"rerank": t_rerank} if second else {})},
     }
     del X
     torch.cuda.empty_cache()
