@@ -185,6 +185,52 @@ ml2_status ml2_rerank(const ml2_ensemble *a, const float *X, int64_t n, int64_t 
                       const int32_t *rows, int32_t m, int32_t keep, float *row_scores,
                       int32_t *out_idx, float *out_score, int32_t *num_selected, void *stream);
 
+/*
+ * The configuration explorer's rounds over one pool (Section 2: the
+ * explorer proposes N configurations per iteration; it applies V and P until
+ * (alpha+1)*N are held and model A keeps N; configurations proposed before
+ * are not proposed again).  An explorer owns the device buffers of one pool
+ * of n candidates (mask, scores, top-k state, the list of proposed rows) and
+ * refers to, but does not own, its ensembles, which must outlive it.
+ *   v, p: validity and performance ensembles; a: second-level ensemble or
+ *   NULL (then the k held rows keep P's order); k = (alpha+1)*N rows held
+ *   per round, keep = N rows proposed per round, max_rounds rounds before a
+ *   reset.  Allocates device memory on the current device (synchronously).
+ * Errors: INVALID_ARG (NULL out/v/p, n < 1, keep < 1 or > k, max_rounds < 1,
+ * ensembles on another device), UNSUPPORTED (k > ML2_MAX_TOPK),
+ * OUT_OF_MEMORY, HIP.
+ */
+typedef struct ml2_explorer ml2_explorer;
+ml2_status ml2_explorer_create(const ml2_ensemble *v, const ml2_ensemble *p,
+                               const ml2_ensemble *a, int64_t n, int32_t k, int32_t keep,
+                               int32_t max_rounds, ml2_explorer **out);
+/* Waits for the device, then releases the explorer's memory (NULL is a no-op). */
+void ml2_explorer_free(ml2_explorer *ex);
+/* Forgets every proposed row and the stored scores (INVALID_ARG if NULL). */
+ml2_status ml2_explorer_reset(ml2_explorer *ex);
+/* Rounds run since creation or the last reset (-1 for NULL). */
+int32_t ml2_explorer_rounds(const ml2_explorer *ex);
+
+/*
+ * One round over the pool X (float32 [n][ld] device, ld >= every ensemble's
+ * feature count, the same pool in every round):
+ *   1. with rescore != 0 (the models changed) or in the first round:
+ *      validity mask and performance scores of every row, as
+ *      ml2_score_validity and ml2_score_perf; otherwise the stored ones;
+ *   2. rows proposed in earlier rounds leave the mask;
+ *   3. the k best remaining accepted rows, as ml2_filter_topk;
+ *   4. the keep best of those by model A's score (or by P's without A),
+ *      as ml2_rerank; written to out_idx/out_score (int32/float32 [keep],
+ *      device; -1/-inf padding once the pool runs dry), *num_selected
+ *      (int32, device), and recorded as proposed.
+ * All of it is enqueued on `stream`; nothing waits for the device.  Calls
+ * on one explorer must not overlap.  Errors: INVALID_ARG (NULL pointers,
+ * ld too small, misaligned X, every round used), UNSUPPORTED, HIP.
+ */
+ml2_status ml2_explorer_round(ml2_explorer *ex, const float *X, int64_t ld, int32_t rescore,
+                              int32_t *out_idx, float *out_score, int32_t *num_selected,
+                              void *stream);
+
 /* Thread-local description of the last non-OK status on this thread. */
 const char *ml2_last_error(void);
 

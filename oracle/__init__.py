@@ -195,6 +195,31 @@ def rerank(a_ens, X, rows, keep: int):
     return row_scores[:m], idx[:keep], out[:keep], int(sel)
 
 
+def explore(v_ens, p_ens, a_ens, X, k: int, keep: int, rounds: int, threads: int = 1):
+    """The explorer's rounds over a fixed pool with fixed models (Section 2):
+    each round holds the k best accepted rows not proposed before (by P),
+    model A (or P's order when a_ens is None) keeps `keep` of them, and those
+    are proposed.  Returns [(idx i32 [keep], score f32 [keep], num)] per
+    round; -1/-inf pad a round once the pool runs dry; a zero score is
+    reported as +0.0."""
+    valid, _ = validity(v_ens, X, threads)
+    score = perf(p_ens, X, valid, threads)
+    proposed = np.zeros(valid.shape[0], bool)
+    out = []
+    for _ in range(rounds):
+        mask = (valid != 0) & ~proposed
+        held, held_score, n_held = topk(mask.astype(np.uint8), score, k)
+        if a_ens is not None:
+            _, idx, top, num = rerank(a_ens, X, held, keep)
+        else:
+            idx, top = held[:keep].copy(), held_score[:keep].copy()
+            top[top == 0] = 0.0
+            num = min(n_held, keep)
+        proposed[idx[idx >= 0]] = True
+        out.append((idx, top, num))
+    return out
+
+
 def pipeline(v_ens, p_ens, X, k: int, threads: int = 1):
     """Validity -> masked performance -> top-k, as the explorer applies them."""
     valid, marg = validity(v_ens, X, threads)

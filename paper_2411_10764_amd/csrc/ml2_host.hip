@@ -19,6 +19,25 @@ struct ml2_ensemble {
   ml2::Forest f;
 };
 
+// Device state of an explorer over one pool (see ml2_explorer_create).
+struct ml2_explorer {
+  const ml2_ensemble *v, *p, *a;  // not owned
+  int device;
+  int64_t n;
+  int32_t k, keep, max_rounds, rounds;
+  bool scored;  // valid/score hold the models' view of the pool
+  void *block;  // one allocation holding every buffer below
+  uint8_t *valid;
+  float *score;
+  int32_t *tk_idx;
+  float *tk_score;
+  int32_t *tk_num;
+  float *a_scores;
+  int32_t *proposed;  // [max_rounds * keep] rows proposed so far (-1 padding)
+  void *ws;
+  size_t ws_bytes;
+};
+
 namespace {
 
 thread_local std::string g_last_error;
@@ -384,6 +403,146 @@ ml2_status ml2_rerank(const ml2_ensemble *a, const float *X, int64_t n, int64_t 
   hipError_t e = ml2::launch_rerank_select(rows, row_scores, m, n, keep, out_idx, out_score,
                                            num_selected, s);
   if (e != hipSuccess) return hip_fail(e, "rerank select launch");
+  return ML2_OK;
+}
+
+ml2_status ml2_explorer_create(const ml2_ensemble *v, const ml2_ensemble *p,
+                               const ml2_ensemble *a, int64_t n, int32_t k, int32_t keep,
+                               int32_t max_rounds, ml2_explorer **out) {
+  if (!out) return fail(ML2_ERR_INVALID_ARG, "ml2_explorer_create: out is NULL");
+  *out = nullptr;
+  if (!v || !p) return fail(ML2_ERR_INVALID_ARG, "ml2_explorer_create: NULL V or P ensemble");
+  if (n < 1 || n > (int64_t)INT32_MAX)
+    return fail(ML2_ERR_INVALID_ARG, "ml2_explorer_create: n = %lld outside [1, 2^31-1]",
+                (long long)n);
+  if (k < 1 || keep < 1 || keep > k || max_rounds < 1)
+    return fail(ML2_ERR_INVALID_ARG,
+                "ml2_explorer_create: need 1 <= keep <= k and max_rounds >= 1 (k = %d, keep = "
+                "%d, max_rounds = %d)", k, keep, max_rounds);
+  if (k > ML2_MAX_TOPK)
+    return fail(ML2_ERR_UNSUPPORTED, "ml2_explorer_create: k = %d > %d", k, ML2_MAX_TOPK);
+  if ((int64_t)max_rounds * keep > (int64_t)INT32_MAX)
+    return fail(ML2_ERR_INVALID_ARG, "ml2_explorer_create: max_rounds * keep overflows");
+  int dev = 0;
+  ml2_status st = current_device(&dev);
+  if (st != ML2_OK) return st;
+  if (v->f.device != dev || p->f.device != dev || (a && a->f.device != dev))
+    return fail(ML2_ERR_INVALID_ARG, "ml2_explorer_create: ensembles not on device %d", dev);
+  auto up = [](size_t b) { return (b + 255) & ~(size_t)255; };
+  const size_t ws = ml2::topk_workspace_bytes(n, k);
+  const size_t sizes[] = {up((size_t)n), up(4 * (size_t)n), up(4 * (size_t)k), up(4 * (size_t)k),
+                          up(4), up(4 * (size_t)k), up(4 * (size_t)max_rounds * keep), up(ws)};
+  size_t total = 0;
+  for (size_t b : sizes) total += b;
+  ml2_explorer *ex = new (std::nothrow) ml2_explorer{};
+  if (!ex) return fail(ML2_ERR_OUT_OF_MEMORY, "ml2_explorer_create: handle allocation failed");
+  hipError_t e = hipMalloc(&ex->block, total);
+  if (e != hipSuccess) {
+    delete ex;
+    if (e == hipErrorOutOfMemory)
+      return fail(ML2_ERR_OUT_OF_MEMORY, "ml2_explorer_create: hipMalloc(%zu)", total);
+    return hip_fail(e, "ml2_explorer_create: hipMalloc");
+  }
+  char *c = static_cast<char *>(ex->block);
+  ex->valid = reinterpret_cast<uint8_t *>(c);            c += sizes[0];
+  ex->score = reinterpret_cast<float *>(c);              c += sizes[1];
+  ex->tk_idx = reinterpret_cast<int32_t *>(c);           c += sizes[2];
+  ex->tk_score = reinterpret_cast<float *>(c);           c += sizes[3];
+  ex->tk_num = reinterpret_cast<int32_t *>(c);           c += sizes[4];
+  ex->a_scores = reinterpret_cast<float *>(c);           c += sizes[5];
+  ex->proposed = reinterpret_cast<int32_t *>(c);         c += sizes[6];
+  ex->ws = c;
+  ex->ws_bytes = sizes[7];
+  ex->v = v;
+  ex->p = p;
+  ex->a = a;
+  ex->device = dev;
+  ex->n = n;
+  ex->k = k;
+  ex->keep = keep;
+  ex->max_rounds = max_rounds;
+  ex->rounds = 0;
+  ex->scored = false;
+  *out = ex;
+  return ML2_OK;
+}
+
+void ml2_explorer_free(ml2_explorer *ex) {
+  if (!ex) return;
+  int cur = 0;
+  const bool other = hipGetDevice(&cur) == hipSuccess && cur != ex->device;
+  if (other) (void)hipSetDevice(ex->device);
+  (void)hipDeviceSynchronize();
+  (void)hipFree(ex->block);
+  if (other) (void)hipSetDevice(cur);
+  delete ex;
+}
+
+ml2_status ml2_explorer_reset(ml2_explorer *ex) {
+  if (!ex) return fail(ML2_ERR_INVALID_ARG, "ml2_explorer_reset: explorer is NULL");
+  ex->rounds = 0;
+  ex->scored = false;
+  return ML2_OK;
+}
+
+int32_t ml2_explorer_rounds(const ml2_explorer *ex) { return ex ? ex->rounds : -1; }
+
+ml2_status ml2_explorer_round(ml2_explorer *ex, const float *X, int64_t ld, int32_t rescore,
+                              int32_t *out_idx, float *out_score, int32_t *num_selected,
+                              void *stream) {
+  if (!ex) return fail(ML2_ERR_INVALID_ARG, "ml2_explorer_round: explorer is NULL");
+  if (!out_idx || !out_score || !num_selected)
+    return fail(ML2_ERR_INVALID_ARG, "ml2_explorer_round: NULL output array");
+  if (ex->rounds >= ex->max_rounds)
+    return fail(ML2_ERR_INVALID_ARG, "ml2_explorer_round: all %d rounds used (reset first)",
+                ex->max_rounds);
+  int dev = 0;
+  const ml2_ensemble *models[3] = {ex->v, ex->p, ex->a};
+  for (const ml2_ensemble *m : models) {
+    if (!m) continue;
+    ml2_status st = check_stream_args(m, X, ex->n, ld, X, "ml2_explorer_round", &dev);
+    if (st != ML2_OK) return st;
+  }
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const int cus = cu_count(dev);
+  const int32_t held = ex->rounds * ex->keep;  // rows proposed in earlier rounds
+  hipError_t e = hipSuccess;
+  if (rescore || !ex->scored) {
+    ml2::WalkPlan pv, pp;
+    const char *why = nullptr;
+    if (!ml2::plan_walk(ex->v->f, ex->n, cus, &pv, &why) ||
+        !ml2::plan_walk(ex->p->f, ex->n, cus, &pp, &why))
+      return fail(ML2_ERR_UNSUPPORTED, "ml2_explorer_round: %s", why);
+    e = ml2::launch_validity(ex->v->f, pv, X, ex->n, ld, ex->valid, nullptr, s);
+    if (e == hipSuccess) e = ml2::launch_exclude(ex->valid, ex->n, ex->proposed, held, s);
+    if (e == hipSuccess) e = ml2::launch_perf(ex->p->f, pp, X, ex->n, ld, ex->valid, ex->score, s);
+    if (e != hipSuccess) return hip_fail(e, "explorer scoring launch");
+  } else if (ex->rounds > 0) {
+    // same scores: only the previous round's rows leave the pool
+    e = ml2::launch_exclude(ex->valid, ex->n, ex->proposed + held - ex->keep, ex->keep, s);
+    if (e != hipSuccess) return hip_fail(e, "explorer exclusion launch");
+  }
+  e = ml2::launch_topk(ex->valid, ex->score, ex->n, ex->k, ex->tk_idx, ex->tk_score, ex->tk_num,
+                       ex->ws, cus, s);
+  if (e != hipSuccess) return hip_fail(e, "explorer top-k launch");
+  const float *by = ex->tk_score;  // without model A the k held keep their P order
+  if (ex->a) {
+    ml2::WalkPlan pa;
+    const char *why = nullptr;
+    if (!ml2::plan_walk(ex->a->f, ex->k, cus, &pa, &why))
+      return fail(ML2_ERR_UNSUPPORTED, "ml2_explorer_round: %s", why);
+    e = ml2::launch_rows(ex->a->f, pa, X, ex->n, ld, ex->tk_idx, ex->k, ex->a_scores, s);
+    if (e != hipSuccess) return hip_fail(e, "explorer re-rank launch");
+    by = ex->a_scores;
+  }
+  e = ml2::launch_rerank_select(ex->tk_idx, by, ex->k, ex->n, ex->keep, out_idx, out_score,
+                                num_selected, s);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(ex->proposed + held, out_idx, sizeof(int32_t) * ex->keep,
+                       hipMemcpyDeviceToDevice, s);
+  if (e != hipSuccess) return hip_fail(e, "explorer selection launch");
+  ex->rounds += 1;
+  ex->scored = true;
   return ML2_OK;
 }
 

@@ -72,6 +72,10 @@ hipError_t launch_topk(const uint8_t *valid, const float *scores, int64_t n, int
                        int32_t *idx, float *score, int32_t *num, void *ws, int cu_count,
                        hipStream_t s);
 
+// mask[rows[j]] = 0 for the listed rows inside [0, n).
+hipError_t launch_exclude(uint8_t *mask, int64_t n, const int32_t *rows, int32_t m,
+                          hipStream_t s);
+
 // The `keep` best of m listed rows by (score desc, pool row asc); m <= ML2_MAX_TOPK.
 hipError_t launch_rerank_select(const int32_t *rows, const float *scores, int32_t m, int64_t n,
                                 int32_t keep, int32_t *idx, float *score, int32_t *num,

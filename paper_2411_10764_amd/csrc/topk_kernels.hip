@@ -295,6 +295,16 @@ __global__ void __launch_bounds__(kSortThreads) rerank_select(const int32_t *row
   if (threadIdx.x == 0) *num = cnt;
 }
 
+// Rows already proposed leave the pool: mask[rows[j]] = 0 for the listed rows
+// inside [0, n) (the -1 padding of short rounds is skipped).
+__global__ void __launch_bounds__(256) exclude_rows(uint8_t *mask, int64_t n,
+                                                    const int32_t *rows, int32_t m) {
+  const int32_t j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= m) return;
+  const int32_t r = rows[j];
+  if (r >= 0 && r < n) mask[r] = 0;
+}
+
 }  // namespace
 
 size_t topk_workspace_bytes(int64_t n, int32_t k) {
@@ -350,6 +360,14 @@ hipError_t launch_rerank_select(const int32_t *rows, const float *scores, int32_
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(rerank_select, dim3(1), dim3(kSortThreads), lds, s, rows, scores, m, n, keep,
                      idx, score, num);
+  return hipGetLastError();
+}
+
+hipError_t launch_exclude(uint8_t *mask, int64_t n, const int32_t *rows, int32_t m,
+                          hipStream_t s) {
+  if (m <= 0) return hipSuccess;
+  hipLaunchKernelGGL(exclude_rows, dim3((unsigned)((m + 255) / 256)), dim3(256), 0, s, mask, n,
+                     rows, m);
   return hipGetLastError();
 }
 

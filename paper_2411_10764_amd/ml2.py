@@ -29,7 +29,8 @@ EXPORTED = (
     "ml2_load_ensemble", "ml2_free_ensemble", "ml2_ensemble_num_features",
     "ml2_ensemble_num_trees", "ml2_ensemble_depth", "ml2_score_validity",
     "ml2_score_perf", "ml2_topk_workspace_bytes", "ml2_filter_topk", "ml2_rerank",
-    "ml2_last_error",
+    "ml2_explorer_create", "ml2_explorer_free", "ml2_explorer_reset", "ml2_explorer_rounds",
+    "ml2_explorer_round", "ml2_last_error",
 )
 
 
@@ -82,6 +83,16 @@ def lib():
         L.ml2_filter_topk.argtypes = [P, P, I64, I32, P, P, P, P, SZ, P]
         L.ml2_rerank.restype = I32
         L.ml2_rerank.argtypes = [P, P, I64, I64, P, I32, I32, P, P, P, P, P]
+        L.ml2_explorer_create.restype = I32
+        L.ml2_explorer_create.argtypes = [P, P, P, I64, I32, I32, I32, ctypes.POINTER(P)]
+        L.ml2_explorer_free.restype = None
+        L.ml2_explorer_free.argtypes = [P]
+        L.ml2_explorer_reset.restype = I32
+        L.ml2_explorer_reset.argtypes = [P]
+        L.ml2_explorer_rounds.restype = I32
+        L.ml2_explorer_rounds.argtypes = [P]
+        L.ml2_explorer_round.restype = I32
+        L.ml2_explorer_round.argtypes = [P, P, I64, I32, P, P, P, P]
         L.ml2_last_error.restype = ctypes.c_char_p
         L.ml2_last_error.argtypes = []
         _lib = L
@@ -219,6 +230,46 @@ def ml2_rerank(a: Ensemble, X, rows, keep: int, row_scores, out_idx, out_score, 
     _check(lib().ml2_rerank(a.handle, xp, n, ld, _ptr(rows), m, keep, _ptr(row_scores),
                             _ptr(out_idx), _ptr(out_score), _ptr(num_selected),
                             _stream(stream)))
+
+
+class Explorer:
+    """An ml2_explorer over one pool of n candidates (owns the handle; holds
+    references to its ensembles so they outlive it)."""
+
+    def __init__(self, v: Ensemble, p: Ensemble, a: Ensemble | None, n: int, k: int,
+                 keep: int, max_rounds: int):
+        h = ctypes.c_void_p()
+        _check(lib().ml2_explorer_create(v.handle, p.handle, a.handle if a else None, n, k, keep,
+                                         max_rounds, ctypes.byref(h)))
+        self.handle = h.value
+        self.models = (v, p, a)
+        self.n, self.k, self.keep = n, k, keep
+
+    @property
+    def rounds(self) -> int:
+        return lib().ml2_explorer_rounds(self.handle)
+
+    def reset(self) -> None:
+        _check(lib().ml2_explorer_reset(self.handle))
+
+    def round(self, X, out_idx, out_score, num_selected, rescore: bool = True,
+              stream=None) -> None:
+        xp, n, ld = _rows(X)
+        if n != self.n:
+            raise ValueError(f"pool has {n} rows, the explorer was made for {self.n}")
+        _check(lib().ml2_explorer_round(self.handle, xp, ld, 1 if rescore else 0, _ptr(out_idx),
+                                        _ptr(out_score), _ptr(num_selected), _stream(stream)))
+
+    def free(self) -> None:
+        if self.handle:
+            lib().ml2_explorer_free(self.handle)
+            self.handle = None
+
+    def __del__(self):  # pragma: no cover - interpreter shutdown order
+        try:
+            self.free()
+        except Exception:
+            pass
 
 
 class Pipeline:

@@ -179,3 +179,18 @@ def test_rerank_null_ensemble():
     P = 1 << 20  # never dereferenced: the NULL ensemble fails validation first
     assert L.ml2_rerank(None, P, 10, 4, P, 5, 3, P, P, P, P, None) == ml2.ML2_ERR_INVALID_ARG
     assert b"NULL" in L.ml2_last_error()
+
+
+def test_explorer_null_handles():
+    import ctypes
+    L = ml2.lib()
+    h = ctypes.c_void_p()
+    assert L.ml2_explorer_create(None, None, None, 10, 4, 2, 3, ctypes.byref(h)) == \
+        ml2.ML2_ERR_INVALID_ARG
+    assert h.value is None
+    assert L.ml2_explorer_create(None, None, None, 10, 4, 2, 3, None) == ml2.ML2_ERR_INVALID_ARG
+    P = 1 << 20  # never dereferenced
+    assert L.ml2_explorer_round(None, P, 8, 1, P, P, P, None) == ml2.ML2_ERR_INVALID_ARG
+    assert L.ml2_explorer_reset(None) == ml2.ML2_ERR_INVALID_ARG
+    assert L.ml2_explorer_rounds(None) == -1
+    L.ml2_explorer_free(None)
