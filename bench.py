@@ -155,6 +155,8 @@ def main() -> int:
         a_idx = torch.empty(w.keep, dtype=torch.int32, device=dev)
         a_top = torch.empty(w.keep, dtype=torch.float32, device=dev)
         a_num = torch.empty(1, dtype=torch.int32, device=dev)
+        a_wsb = ml2.ml2_rerank_workspace_bytes(a, w.k)
+        a_ws = torch.empty(a_wsb, dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
 
     def step(e=None):
@@ -171,8 +173,8 @@ def main() -> int:
         if e is not None:
             e[3].record(stream)
         if second:
-            ml2.ml2_rerank(a, X, pipe.idx, w.keep, a_scores, a_idx, a_top, a_num, m=w.k,
-                           stream=stream)
+            ml2.ml2_rerank(a, X, pipe.idx, w.keep, a_scores, a_idx, a_top, a_num, a_ws, a_wsb,
+                           m=w.k, stream=stream)
         if e is not None:
             e[4].record(stream)
 

@@ -177,13 +177,24 @@ ml2_status ml2_filter_topk(const uint8_t *valid, const float *scores, int64_t n,
  * more columns than those V and P use); rows: int32 [m] device, e.g. the
  * topk_idx of ml2_filter_topk (its -1 padding is skipped); row_scores:
  * float32 [m] device; out_idx: int32 [keep], out_score: float32 [keep],
- * num_selected: int32 [1], all device.  No workspace.
+ * num_selected: int32 [1], all device; workspace: at least
+ * ml2_rerank_workspace_bytes(a, m) bytes of device memory, used by this
+ * call until it completes.  The trees are walked in parallel over the
+ * listed rows (a few rows still occupy the whole GPU) and each row's leaves
+ * are then added in tree order.
  * Errors: INVALID_ARG (NULL pointers, m < 0, keep < 0, n out of range,
- * ld < F, misaligned X), UNSUPPORTED (m or keep > ML2_MAX_TOPK), HIP.
+ * ld < F, misaligned X, small workspace), UNSUPPORTED (m or keep >
+ * ML2_MAX_TOPK), HIP.
  */
 ml2_status ml2_rerank(const ml2_ensemble *a, const float *X, int64_t n, int64_t ld,
                       const int32_t *rows, int32_t m, int32_t keep, float *row_scores,
-                      int32_t *out_idx, float *out_score, int32_t *num_selected, void *stream);
+                      int32_t *out_idx, float *out_score, int32_t *num_selected,
+                      void *workspace, size_t workspace_bytes, void *stream);
+
+/* Device workspace bytes ml2_rerank needs for m listed rows of ensemble a
+ * (one float per tree and row).  Errors: INVALID_ARG (NULL a or bytes,
+ * m < 0), UNSUPPORTED (m > ML2_MAX_TOPK). */
+ml2_status ml2_rerank_workspace_bytes(const ml2_ensemble *a, int32_t m, size_t *bytes);
 
 /*
  * The configuration explorer's rounds over one pool (Section 2: the

@@ -5,5 +5,5 @@ selected ones, behind the C ABI of
 include/ml2.h (libml2.so) and the thin ctypes binding in ``ml2``."""
 from .ml2 import (  # noqa: F401
     Ensemble, Explorer, Ml2Error, Pipeline, ml2_filter_topk, ml2_free_ensemble, ml2_load_ensemble,
-    ml2_rerank, ml2_score_perf, ml2_score_validity, ml2_topk_workspace_bytes,
+    ml2_rerank, ml2_rerank_workspace_bytes, ml2_score_perf, ml2_score_validity, ml2_topk_workspace_bytes,
 )

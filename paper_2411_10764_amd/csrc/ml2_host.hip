@@ -34,8 +34,9 @@ struct ml2_explorer {
   int32_t *tk_num;
   float *a_scores;
   int32_t *proposed;  // [max_rounds * keep] rows proposed so far (-1 padding)
-  void *ws;
+  void *ws;           // top-k workspace
   size_t ws_bytes;
+  void *a_ws;         // second-level leaves
 };
 
 namespace {
@@ -370,9 +371,19 @@ ml2_status ml2_filter_topk(const uint8_t *valid, const float *scores, int64_t n,
   return ML2_OK;
 }
 
+ml2_status ml2_rerank_workspace_bytes(const ml2_ensemble *a, int32_t m, size_t *bytes) {
+  if (!a || !bytes) return fail(ML2_ERR_INVALID_ARG, "ml2_rerank_workspace_bytes: NULL argument");
+  if (m < 0) return fail(ML2_ERR_INVALID_ARG, "ml2_rerank_workspace_bytes: m = %d < 0", m);
+  if (m > ML2_MAX_TOPK)
+    return fail(ML2_ERR_UNSUPPORTED, "ml2_rerank_workspace_bytes: m = %d > %d", m, ML2_MAX_TOPK);
+  *bytes = ml2::rows_workspace_bytes(a->f, m);
+  return ML2_OK;
+}
+
 ml2_status ml2_rerank(const ml2_ensemble *a, const float *X, int64_t n, int64_t ld,
                       const int32_t *rows, int32_t m, int32_t keep, float *row_scores,
-                      int32_t *out_idx, float *out_score, int32_t *num_selected, void *stream) {
+                      int32_t *out_idx, float *out_score, int32_t *num_selected,
+                      void *workspace, size_t workspace_bytes, void *stream) {
   int dev = 0;
   ml2_status st = check_stream_args(a, X, n, ld, X, "ml2_rerank", &dev);
   if (st != ML2_OK) return st;
@@ -386,13 +397,14 @@ ml2_status ml2_rerank(const ml2_ensemble *a, const float *X, int64_t n, int64_t 
     return fail(ML2_ERR_INVALID_ARG, "ml2_rerank: NULL rows or row_scores");
   if (keep > 0 && (!out_idx || !out_score))
     return fail(ML2_ERR_INVALID_ARG, "ml2_rerank: NULL output array");
+  const size_t need = ml2::rows_workspace_bytes(a->f, m);
+  if (m > 0 && n > 0 && (!workspace || workspace_bytes < need))
+    return fail(ML2_ERR_INVALID_ARG, "ml2_rerank: workspace %zu < %zu bytes", workspace_bytes,
+                need);
   const hipStream_t s = static_cast<hipStream_t>(stream);
   if (m > 0 && n > 0) {
-    ml2::WalkPlan p;
-    const char *why = nullptr;
-    if (!ml2::plan_walk(a->f, m, cu_count(dev), &p, &why))
-      return fail(ML2_ERR_UNSUPPORTED, "ml2_rerank: %s", why);
-    hipError_t e = ml2::launch_rows(a->f, p, X, n, ld, rows, m, row_scores, s);
+    hipError_t e = ml2::launch_rows(a->f, X, n, ld, rows, m, row_scores, workspace, cu_count(dev),
+                                    s);
     if (e != hipSuccess) return hip_fail(e, "rerank walk launch");
   }
   if (m > 0 && n == 0) {  // no listed row is in range (and X may be NULL)
@@ -430,8 +442,10 @@ ml2_status ml2_explorer_create(const ml2_ensemble *v, const ml2_ensemble *p,
     return fail(ML2_ERR_INVALID_ARG, "ml2_explorer_create: ensembles not on device %d", dev);
   auto up = [](size_t b) { return (b + 255) & ~(size_t)255; };
   const size_t ws = ml2::topk_workspace_bytes(n, k);
+  const size_t a_ws = a ? ml2::rows_workspace_bytes(a->f, k) : 0;
   const size_t sizes[] = {up((size_t)n), up(4 * (size_t)n), up(4 * (size_t)k), up(4 * (size_t)k),
-                          up(4), up(4 * (size_t)k), up(4 * (size_t)max_rounds * keep), up(ws)};
+                          up(4), up(4 * (size_t)k), up(4 * (size_t)max_rounds * keep), up(ws),
+                          up(a_ws)};
   size_t total = 0;
   for (size_t b : sizes) total += b;
   ml2_explorer *ex = new (std::nothrow) ml2_explorer{};
@@ -451,8 +465,9 @@ ml2_status ml2_explorer_create(const ml2_ensemble *v, const ml2_ensemble *p,
   ex->tk_num = reinterpret_cast<int32_t *>(c);           c += sizes[4];
   ex->a_scores = reinterpret_cast<float *>(c);           c += sizes[5];
   ex->proposed = reinterpret_cast<int32_t *>(c);         c += sizes[6];
-  ex->ws = c;
+  ex->ws = c;                                            c += sizes[7];
   ex->ws_bytes = sizes[7];
+  ex->a_ws = c;
   ex->v = v;
   ex->p = p;
   ex->a = a;
@@ -527,11 +542,8 @@ ml2_status ml2_explorer_round(ml2_explorer *ex, const float *X, int64_t ld, int3
   if (e != hipSuccess) return hip_fail(e, "explorer top-k launch");
   const float *by = ex->tk_score;  // without model A the k held keep their P order
   if (ex->a) {
-    ml2::WalkPlan pa;
-    const char *why = nullptr;
-    if (!ml2::plan_walk(ex->a->f, ex->k, cus, &pa, &why))
-      return fail(ML2_ERR_UNSUPPORTED, "ml2_explorer_round: %s", why);
-    e = ml2::launch_rows(ex->a->f, pa, X, ex->n, ld, ex->tk_idx, ex->k, ex->a_scores, s);
+    e = ml2::launch_rows(ex->a->f, X, ex->n, ld, ex->tk_idx, ex->k, ex->a_scores, ex->a_ws, cus,
+                         s);
     if (e != hipSuccess) return hip_fail(e, "explorer re-rank launch");
     by = ex->a_scores;
   }

@@ -62,10 +62,12 @@ hipError_t launch_validity(const Forest &f, const WalkPlan &p, const float *X, i
 hipError_t launch_perf(const Forest &f, const WalkPlan &p, const float *X, int64_t n,
                        int64_t ld, const uint8_t *valid, float *score_out, hipStream_t s);
 
-// Perf walk over a list of pool rows: score_out[i] = margin of row rows[i],
-// or -inf where rows[i] lies outside [0, n).
-hipError_t launch_rows(const Forest &f, const WalkPlan &p, const float *X, int64_t n, int64_t ld,
-                       const int32_t *rows, int32_t m, float *score_out, hipStream_t s);
+// Walk of a list of pool rows: score_out[i] = margin of row rows[i], or -inf
+// where rows[i] lies outside [0, n).  ws: rows_workspace_bytes(f, m) bytes
+// of device memory (the per-tree leaves).
+size_t rows_workspace_bytes(const Forest &f, int32_t m);
+hipError_t launch_rows(const Forest &f, const float *X, int64_t n, int64_t ld, const int32_t *rows,
+                       int32_t m, float *score_out, void *ws, int cu_count, hipStream_t s);
 
 size_t topk_workspace_bytes(int64_t n, int32_t k);
 hipError_t launch_topk(const uint8_t *valid, const float *scores, int64_t n, int32_t k,

@@ -32,6 +32,8 @@
 #include <math.h>
 #include <stdlib.h>
 
+#include <algorithm>
+
 #include "ml2_internal.h"
 
 namespace ml2 {
@@ -56,7 +58,7 @@ struct Geo {
 
 struct WalkArgs {
   const float *X;
-  int64_t n;            // entries walked: pool rows, or list positions
+  int64_t n;            // entries: pool rows, or list entries
   int64_t n_pool;       // rows of X
   int64_t ld;
   const char *trees;
@@ -77,16 +79,10 @@ struct WalkArgs {
   uint8_t *valid_out;   // validity
   float *margin_out;
   const uint8_t *valid_in;  // perf
-  const int32_t *rows_in;   // perf over a row list: entry i is pool row rows_in[i]
-  float *score_out;         // perf: one score per entry
+  float *score_out;         // perf; the fold of a row list
+  const int32_t *rows_in;   // row list: entry i is pool row rows_in[i]
+  float *leaves_out;        // leaf walk of a row list: [ntrees][n]
 };
-
-// Pool row of entry `pos` (-1 for none).  List entries outside [0, n_pool)
-// are never queued.
-__device__ __forceinline__ int64_t pool_row(const WalkArgs &a, int32_t pos) {
-  if (pos < 0) return -1;
-  return a.rows_in ? (int64_t)a.rows_in[pos] : (int64_t)pos;
-}
 
 // Row `row` of X into the tile of its candidate (dst = tile + 4*candidate),
 // whole, by one lane.  Pool rows are read with plain loads: a line whose
@@ -309,6 +305,50 @@ struct Walks {
   }
 };
 
+// One group: half-wave h walks the G trees of records starting at `rec`
+// (two halves of H = G/2 offset by half a level), then `done(A, B)` gets the
+// leaves (A: the first H trees, B: the next H; with G == 1 only A).
+template <int D, int G, int S, typename Done>
+__device__ __forceinline__ void walk_group(const char *rec, const char *tile_lane, Done done) {
+  constexpr uint32_t RB = record_bytes(D);
+  if constexpr (G == 1) {
+    Walks<D, 1, S> A;
+    A.start();
+#pragma unroll
+    for (int l = 0; l < D; ++l) {
+      A.read_nodes(rec);
+      A.read_features(tile_lane);
+      A.descend();
+    }
+    A.read_leaves(rec);
+    done(A, A);
+  } else {
+    constexpr int H = G / 2;
+    const char *recA = rec;
+    const char *recB = rec + H * RB;
+    Walks<D, H, S> A, B;
+    A.start();
+    B.start();
+    A.read_nodes(recA);
+    B.read_nodes(recB);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int l = 0; l < D; ++l) {
+      A.read_features(tile_lane);
+      __builtin_amdgcn_sched_barrier(0);
+      B.read_features(tile_lane);
+      __builtin_amdgcn_sched_barrier(0);
+      A.descend();
+      if (l + 1 < D) A.read_nodes(recA); else A.read_leaves(recA);
+      __builtin_amdgcn_sched_barrier(0);
+      B.descend();
+      if (l + 1 < D) B.read_nodes(recB); else B.read_leaves(recB);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    done(A, B);
+  }
+}
+
 // Walk `ntr` trees (a multiple of S*G) of the chunk at `cb`, folding their
 // leaves into m in tree order.  Half-wave h walks trees [t0 + h*G, t0 +
 // (h+1)*G) of each group of S*G; with S = 2 only the lower half's m is the
@@ -318,48 +358,17 @@ __device__ __forceinline__ float walk_chunk(const char *cb, int ntr, const char 
                                             int h, float m) {
   constexpr uint32_t RB = record_bytes(D);
   constexpr int GS = G * S;
-  if constexpr (G == 1) {
-    for (int t0 = 0; t0 < ntr; t0 += GS) {
-      const char *rec = cb + (uint32_t)(t0 + h) * RB;
-      Walks<D, 1, S> A;
-      A.start();
-#pragma unroll
-      for (int l = 0; l < D; ++l) {
-        A.read_nodes(rec);
-        A.read_features(tile_lane);
-        A.descend();
-      }
-      A.read_leaves(rec);
-      m = A.fold(m);
-      if constexpr (S == 2) m = A.fold_upper(m);
-    }
-  } else {
-    constexpr int H = G / 2;
-    for (int t0 = 0; t0 < ntr; t0 += GS) {
-      const char *recA = cb + (uint32_t)(t0 + h * G) * RB;
-      const char *recB = recA + H * RB;
-      Walks<D, H, S> A, B;
-      A.start();
-      B.start();
-      A.read_nodes(recA);
-      B.read_nodes(recB);
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int l = 0; l < D; ++l) {
-        A.read_features(tile_lane);
-        __builtin_amdgcn_sched_barrier(0);
-        B.read_features(tile_lane);
-        __builtin_amdgcn_sched_barrier(0);
-        A.descend();
-        if (l + 1 < D) A.read_nodes(recA); else A.read_leaves(recA);
-        __builtin_amdgcn_sched_barrier(0);
-        B.descend();
-        if (l + 1 < D) B.read_nodes(recB); else B.read_leaves(recB);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-      m = B.fold(A.fold(m));
-      if constexpr (S == 2) m = B.fold_upper(A.fold_upper(m));
-    }
+  for (int t0 = 0; t0 < ntr; t0 += GS) {
+    walk_group<D, G, S>(cb + (uint32_t)(t0 + h * G) * RB, tile_lane,
+                        [&](const auto &A, const auto &B) {
+                          if constexpr (G == 1) {
+                            m = A.fold(m);
+                            if constexpr (S == 2) m = A.fold_upper(m);
+                          } else {
+                            m = B.fold(A.fold(m));
+                            if constexpr (S == 2) m = B.fold_upper(A.fold_upper(m));
+                          }
+                        });
   }
   return m;
 }
@@ -540,13 +549,7 @@ perf_kernel(WalkArgs a) {
     while (qn < C && step < nsteps) {
       const int64_t i = step * NT + threadIdx.x;
       const bool in = i < a.n;
-      bool v = in;
-      if (in && a.rows_in) {
-        const int32_t r = a.rows_in[i];
-        v = r >= 0 && r < a.n_pool;
-      } else if (in && a.valid_in) {
-        v = a.valid_in[i] != 0;
-      }
+      const bool v = in && (a.valid_in == nullptr || a.valid_in[i] != 0);
       if (in && !v) __builtin_nontemporal_store(-INFINITY, a.score_out + i);
       const uint64_t bal = __ballot(v);
       if (lane == 0) wave_count[wave] = __popcll(bal);
@@ -572,25 +575,79 @@ perf_kernel(WalkArgs a) {
     __syncthreads();
     return r;
   };
-  // `pos` is an entry (a pool row, or a list position), `row` its pool row.
   RowHead head;
-  int32_t pos = next_rows();
-  int64_t row = pool_row(a, pos);
+  int32_t row = next_rows();
   if (a.rowpf) row_batch_load(a, row, h, head.v);
   for (;;) {
-    if (__syncthreads_or(pos >= 0) == 0) break;
+    if (__syncthreads_or(row >= 0) == 0) break;
     if (a.rowpf)
       row_commit<S>(a, row, head, h, tile_lane);
     else if (row >= 0 && h == 0)
       load_row<S>(a, row, tile_lane);
-    const int32_t npos = next_rows();  // ends with a barrier: the tiles are complete
-    const int64_t nrow = pool_row(a, npos);
+    const int32_t nrow = next_rows();  // ends with a barrier: the tiles are complete
     if (a.rowpf) row_batch_load(a, nrow, h, head.v);
     const float m = walk_all<D, G, S>(a, st, tile_lane, h);
-    if (pos >= 0 && h == 0) __builtin_nontemporal_store(m, a.score_out + pos);
-    pos = npos;
+    if (row >= 0 && h == 0) __builtin_nontemporal_store(m, a.score_out + row);
     row = nrow;
   }
+}
+
+// Tree-parallel walk of a short row list (the second level): workgroup
+// (c, r) stages tree chunk c once, loads list entries [r*64W, (r+1)*64W)
+// (lane = entry) and writes the leaf each of its trees gives each entry to
+// leaves_out[t * n + entry].  fold_kernel then adds them up in tree order, so
+// a list of a few rows still spreads over the whole GPU.
+template <int D, int G>
+__global__ void __launch_bounds__(kLanes * 4) leaves_kernel(WalkArgs a) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  constexpr uint32_t RB = record_bytes(D);
+  const int lane = threadIdx.x & (kLanes - 1);
+  const int wave = threadIdx.x / kLanes;
+  const int W = a.nthreads / kLanes;
+  const size_t tile_bytes = (size_t)a.F * Geo<1>::kRowBytes;
+  char *chunk = smem + W * tile_bytes;
+  const int t0 = blockIdx.x * a.chunk_trees;
+  const int nt = min(a.chunk_trees, a.ntrees - t0);  // a multiple of G
+  const u32x4 *src = reinterpret_cast<const u32x4 *>(a.trees + (size_t)t0 * RB);
+  for (uint32_t i = threadIdx.x; i < (uint32_t)nt * (RB / 16u); i += a.nthreads)
+    reinterpret_cast<u32x4 *>(chunk)[i] = src[i];
+  const int64_t pos = ((int64_t)blockIdx.y * W + wave) * kLanes + lane;
+  int64_t row = -1;
+  if (pos < a.n) {
+    const int32_t r = a.rows_in[pos];
+    if (r >= 0 && r < a.n_pool) row = r;
+  }
+  char *tile_lane = smem + wave * tile_bytes + 4 * lane;
+  if (row >= 0) load_row<1>(a, row, tile_lane);
+  __syncthreads();
+  for (int g0 = 0; g0 < nt; g0 += G) {
+    walk_group<D, G, 1>(chunk + (uint32_t)g0 * RB, tile_lane, [&](const auto &A, const auto &B) {
+      if (row < 0) return;
+      float *out = a.leaves_out + (size_t)(t0 + g0) * a.n + pos;
+      constexpr int H = G == 1 ? 1 : G / 2;
+#pragma unroll
+      for (int g = 0; g < H; ++g) out[(size_t)g * a.n] = A.leaf[g];
+      if constexpr (G > 1) {
+#pragma unroll
+        for (int g = 0; g < H; ++g) out[(size_t)(H + g) * a.n] = B.leaf[g];
+      }
+    });
+  }
+}
+
+// score_out[i] = base + leaf_0 + leaf_1 + ... (float32, tree order) for list
+// entries whose row is in the pool, -inf for the others.
+__global__ void __launch_bounds__(256) fold_kernel(WalkArgs a) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= a.n) return;
+  const int32_t r = a.rows_in[i];
+  if (r < 0 || r >= a.n_pool) {
+    a.score_out[i] = -INFINITY;
+    return;
+  }
+  float m = a.base;
+  for (int t = 0; t < a.ntrees; ++t) m = m + a.leaves_out[(size_t)t * a.n + i];
+  a.score_out[i] = m;
 }
 
 // Trees walked concurrently per lane that a depth allows.  S = 1: a chunk
@@ -664,6 +721,49 @@ hipError_t launch_walk(bool perf, const Forest &f, const WalkPlan &p, const Walk
     case 10: return launch_depth<10>(perf, p, a, s);
     case 11: return launch_depth<11>(perf, p, a, s);
     case 12: return launch_depth<12>(perf, p, a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <int D, int G>
+hipError_t launch_leaves_dg(const WalkArgs &a, int W, size_t lds, int row_tiles, hipStream_t s) {
+  const void *fn = reinterpret_cast<const void *>(&leaves_kernel<D, G>);
+  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((leaves_kernel<D, G>), dim3((unsigned)a.nchunks, (unsigned)row_tiles),
+                     dim3(W * kLanes), lds, s, a);
+  return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_leaves_depth(const WalkArgs &a, int G, int W, size_t lds, int row_tiles,
+                               hipStream_t s) {
+  switch (G) {
+    case 1: if constexpr (group_allowed(D, 1, 1)) return launch_leaves_dg<D, 1>(a, W, lds, row_tiles, s); break;
+    case 2: if constexpr (group_allowed(D, 2, 1)) return launch_leaves_dg<D, 2>(a, W, lds, row_tiles, s); break;
+    case 4: if constexpr (group_allowed(D, 4, 1)) return launch_leaves_dg<D, 4>(a, W, lds, row_tiles, s); break;
+    case 8: if constexpr (group_allowed(D, 8, 1)) return launch_leaves_dg<D, 8>(a, W, lds, row_tiles, s); break;
+    case 16: if constexpr (group_allowed(D, 16, 1)) return launch_leaves_dg<D, 16>(a, W, lds, row_tiles, s); break;
+    default: break;
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_leaves(int depth, const WalkArgs &a, int G, int W, size_t lds, int row_tiles,
+                         hipStream_t s) {
+  switch (depth) {
+    case 1: return launch_leaves_depth<1>(a, G, W, lds, row_tiles, s);
+    case 2: return launch_leaves_depth<2>(a, G, W, lds, row_tiles, s);
+    case 3: return launch_leaves_depth<3>(a, G, W, lds, row_tiles, s);
+    case 4: return launch_leaves_depth<4>(a, G, W, lds, row_tiles, s);
+    case 5: return launch_leaves_depth<5>(a, G, W, lds, row_tiles, s);
+    case 6: return launch_leaves_depth<6>(a, G, W, lds, row_tiles, s);
+    case 7: return launch_leaves_depth<7>(a, G, W, lds, row_tiles, s);
+    case 8: return launch_leaves_depth<8>(a, G, W, lds, row_tiles, s);
+    case 9: return launch_leaves_depth<9>(a, G, W, lds, row_tiles, s);
+    case 10: return launch_leaves_depth<10>(a, G, W, lds, row_tiles, s);
+    case 11: return launch_leaves_depth<11>(a, G, W, lds, row_tiles, s);
+    case 12: return launch_leaves_depth<12>(a, G, W, lds, row_tiles, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -798,13 +898,60 @@ hipError_t launch_perf(const Forest &f, const WalkPlan &p, const float *X, int64
   return launch_walk(true, f, p, a, s);
 }
 
-hipError_t launch_rows(const Forest &f, const WalkPlan &p, const float *X, int64_t n, int64_t ld,
-                       const int32_t *rows, int32_t m, float *score_out, hipStream_t s) {
-  WalkArgs a = make_args(f, p, X, m, ld);
+size_t rows_workspace_bytes(const Forest &f, int32_t m) {
+  const size_t b = (size_t)f.num_trees_padded * (size_t)(m > 0 ? m : 1) * sizeof(float);
+  return (b + 255) & ~(size_t)255;
+}
+
+// Tree-parallel walk of m listed rows: W waves of 64 entries per workgroup
+// (as many as the list needs, at most four, fewer if the tiles and G trees
+// do not fit), chunks of whole trees sized so the grid holds about two
+// workgroups per CU, then the ordered fold.
+hipError_t launch_rows(const Forest &f, const float *X, int64_t n, int64_t ld, const int32_t *rows,
+                       int32_t m, float *score_out, void *ws, int cu_count, hipStream_t s) {
+  if (m <= 0) return hipSuccess;
+  const size_t rb = f.rec_bytes;
+  const size_t tile = (size_t)f.num_features * Geo<1>::kRowBytes;
+  int W = (int)std::min<int64_t>(4, (m + kLanes - 1) / kLanes);
+  int G = 0;
+  for (; W >= 1; --W) {
+    for (int g : {16, 8, 4, 2, 1}) {
+      if (group_allowed(f.depth, g, 1) && W * tile + g * rb <= kLdsBudget) {
+        G = g;
+        break;
+      }
+    }
+    if (G) break;
+  }
+  if (!G) return hipErrorInvalidValue;  // excluded by the loader's limits
+  const int row_tiles = (int)((m + (int64_t)W * kLanes - 1) / ((int64_t)W * kLanes));
+  const int tpad = f.num_trees_padded;  // a multiple of kTreePad, hence of G
+  int ct = (int)((kLdsBudget - W * tile) / rb) / G * G;
+  const int64_t want = 2 * (int64_t)cu_count;  // workgroups wanted in flight
+  const int64_t chunks_wanted = (want + row_tiles - 1) / row_tiles;
+  const int cap = (int)std::max<int64_t>(G, (tpad / std::max<int64_t>(chunks_wanted, 1)) / G * G);
+  ct = std::min(std::min(ct, cap), tpad);
+  WalkArgs a{};
+  a.X = X;
+  a.n = m;
   a.n_pool = n;
+  a.ld = ld;
+  a.trees = static_cast<const char *>(f.d_trees);
+  a.ntrees = tpad;
+  a.chunk_trees = ct;
+  a.nchunks = (tpad + ct - 1) / ct;
+  a.F = f.num_features;
+  a.vec4 = ((reinterpret_cast<uintptr_t>(X) & 15u) == 0 && (ld & 3) == 0) ? 1 : 0;
+  a.nthreads = W * kLanes;
+  a.base = f.base;
   a.rows_in = rows;
   a.score_out = score_out;
-  return launch_walk(true, f, p, a, s);
+  a.leaves_out = static_cast<float *>(ws);
+  const size_t lds = W * tile + (size_t)ct * rb;
+  hipError_t e = launch_leaves(f.depth, a, G, W, lds, row_tiles, s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(fold_kernel, dim3((unsigned)((m + 255) / 256)), dim3(256), 0, s, a);
+  return hipGetLastError();
 }
 
 }  // namespace ml2

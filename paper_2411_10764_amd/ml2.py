@@ -29,6 +29,7 @@ EXPORTED = (
     "ml2_load_ensemble", "ml2_free_ensemble", "ml2_ensemble_num_features",
     "ml2_ensemble_num_trees", "ml2_ensemble_depth", "ml2_score_validity",
     "ml2_score_perf", "ml2_topk_workspace_bytes", "ml2_filter_topk", "ml2_rerank",
+    "ml2_rerank_workspace_bytes",
     "ml2_explorer_create", "ml2_explorer_free", "ml2_explorer_reset", "ml2_explorer_rounds",
     "ml2_explorer_round", "ml2_last_error",
 )
@@ -82,7 +83,9 @@ def lib():
         L.ml2_filter_topk.restype = I32
         L.ml2_filter_topk.argtypes = [P, P, I64, I32, P, P, P, P, SZ, P]
         L.ml2_rerank.restype = I32
-        L.ml2_rerank.argtypes = [P, P, I64, I64, P, I32, I32, P, P, P, P, P]
+        L.ml2_rerank.argtypes = [P, P, I64, I64, P, I32, I32, P, P, P, P, P, SZ, P]
+        L.ml2_rerank_workspace_bytes.restype = I32
+        L.ml2_rerank_workspace_bytes.argtypes = [P, I32, ctypes.POINTER(SZ)]
         L.ml2_explorer_create.restype = I32
         L.ml2_explorer_create.argtypes = [P, P, P, I64, I32, I32, I32, ctypes.POINTER(P)]
         L.ml2_explorer_free.restype = None
@@ -222,14 +225,23 @@ def ml2_filter_topk(valid, scores, k: int, topk_idx, topk_score, num_selected, w
                                  workspace_bytes, _stream(stream)))
 
 
+def ml2_rerank_workspace_bytes(a: Ensemble, m: int) -> int:
+    out = ctypes.c_size_t()
+    _check(lib().ml2_rerank_workspace_bytes(a.handle, m, ctypes.byref(out)))
+    return int(out.value)
+
+
 def ml2_rerank(a: Ensemble, X, rows, keep: int, row_scores, out_idx, out_score, num_selected,
-               m: int | None = None, stream=None) -> None:
+               workspace, workspace_bytes: int | None = None, m: int | None = None,
+               stream=None) -> None:
     xp, n, ld = _rows(X)
     if m is None:
         m = rows.shape[0]
+    if workspace_bytes is None:
+        workspace_bytes = workspace.numel() * workspace.element_size()
     _check(lib().ml2_rerank(a.handle, xp, n, ld, _ptr(rows), m, keep, _ptr(row_scores),
-                            _ptr(out_idx), _ptr(out_score), _ptr(num_selected),
-                            _stream(stream)))
+                            _ptr(out_idx), _ptr(out_score), _ptr(num_selected), _ptr(workspace),
+                            workspace_bytes, _stream(stream)))
 
 
 class Explorer:

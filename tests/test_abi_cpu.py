@@ -177,8 +177,12 @@ def test_filter_topk_argument_errors():
 def test_rerank_null_ensemble():
     L = ml2.lib()
     P = 1 << 20  # never dereferenced: the NULL ensemble fails validation first
-    assert L.ml2_rerank(None, P, 10, 4, P, 5, 3, P, P, P, P, None) == ml2.ML2_ERR_INVALID_ARG
+    assert L.ml2_rerank(None, P, 10, 4, P, 5, 3, P, P, P, P, P, 1 << 20, None) == \
+        ml2.ML2_ERR_INVALID_ARG
     assert b"NULL" in L.ml2_last_error()
+    import ctypes
+    b = ctypes.c_size_t()
+    assert L.ml2_rerank_workspace_bytes(None, 5, ctypes.byref(b)) == ml2.ML2_ERR_INVALID_ARG
 
 
 def test_explorer_null_handles():

@@ -48,7 +48,9 @@ def rerank_gpu(A, Xd, rows, keep, a=None):
     idx = torch.full((max(keep, 1),), -7, dtype=torch.int32, device=DEV)
     top = torch.empty(max(keep, 1), dtype=torch.float32, device=DEV)
     num = torch.full((1,), -7, dtype=torch.int32, device=DEV)
-    ml2.ml2_rerank(a, Xd, rows_d, keep, rs, idx, top, num, m=m)
+    wsb = ml2.ml2_rerank_workspace_bytes(a, m)
+    ws = torch.full((wsb // 4,), float("nan"), dtype=torch.float32, device=DEV)
+    ml2.ml2_rerank(a, Xd, rows_d, keep, rs, idx, top, num, ws, wsb, m=m)
     torch.cuda.synchronize()
     out = (rs.cpu().numpy()[:m], idx.cpu().numpy()[:keep], top.cpu().numpy()[:keep],
            int(num.item()))
@@ -131,20 +133,21 @@ def test_rerank_max_list():
     check_rerank(A, X, rows, m)
 
 
-@pytest.mark.parametrize("split,waves", [(1, 4), (1, 8), (2, 8), (2, 4)])
-def test_rerank_plans(monkeypatch, split, waves):
-    monkeypatch.setenv("ML2_WALK_SPLIT", str(split))
-    monkeypatch.setenv("ML2_WALK_WAVES", str(waves))
-    rng = np.random.default_rng(11)
-    n, F, K = 3000, 40, 20
+@pytest.mark.parametrize("m", [1, 20, 64, 65, 129, 200, 700, 5000])
+def test_rerank_list_sizes(m):
+    """List sizes that change the leaf walk's waves per workgroup (1..4), its
+    row tiles and its tree-chunk size."""
+    rng = np.random.default_rng(11 + m)
+    n, F, K = 6000, 40, 20
     A = gen.perfect_ensemble(46, 3, 90, 7, F, K, 0.1)
     X = gen.features(46, n, F, K)
-    rows = rng.integers(0, n, 700).astype(np.int32)
-    _note(f"plan S={split} W={waves}")
-    check_rerank(A, X, rows, 100)
+    rows = rng.integers(-2, n, m).astype(np.int32)
+    _note(f"list m={m}")
+    check_rerank(A, X, rows, min(m, 50))
 
 
-@pytest.mark.parametrize("depth,F,ld", [(12, 128, 128), (10, 64, 67), (3, 5, 5)])
+@pytest.mark.parametrize("depth,F,ld", [(12, 128, 128), (12, 256, 256), (10, 64, 67), (8, 128, 130),
+                                         (3, 5, 5), (1, 1, 1)])
 def test_rerank_shapes(depth, F, ld):
     """The explorer's A shape (depth 12 over 128 columns), a ragged row stride,
     and a narrow pool."""
@@ -166,12 +169,15 @@ def test_rerank_argument_errors():
     P = buf.data_ptr()
     xp = X.data_ptr()
     s = torch.cuda.current_stream().cuda_stream
-    ok = dict(n=10, ld=8, rows=P, m=5, keep=3, rs=P, idx=P, sc=P, num=P)
+    wsb = ml2.ml2_rerank_workspace_bytes(a, 5)
+    ws = torch.zeros(wsb, dtype=torch.uint8, device=DEV)
+    ok = dict(n=10, ld=8, rows=P, m=5, keep=3, rs=P, idx=P, sc=P, num=P, ws=ws.data_ptr(),
+              wsb=wsb)
 
     def call(**kw):
         c = dict(ok, **kw)
         return L.ml2_rerank(a.handle, xp, c["n"], c["ld"], c["rows"], c["m"], c["keep"], c["rs"],
-                            c["idx"], c["sc"], c["num"], s)
+                            c["idx"], c["sc"], c["num"], c["ws"], c["wsb"], s)
 
     assert call(m=-1) == ml2.ML2_ERR_INVALID_ARG
     assert call(keep=-1) == ml2.ML2_ERR_INVALID_ARG
@@ -180,8 +186,18 @@ def test_rerank_argument_errors():
     assert call(rows=None) == ml2.ML2_ERR_INVALID_ARG
     assert call(rs=None) == ml2.ML2_ERR_INVALID_ARG
     assert call(idx=None) == ml2.ML2_ERR_INVALID_ARG
+    assert call(ws=None) == ml2.ML2_ERR_INVALID_ARG
+    assert call(wsb=wsb - 1) == ml2.ML2_ERR_INVALID_ARG
     assert call(m=ml2.ML2_MAX_TOPK + 1) == ml2.ML2_ERR_UNSUPPORTED
     assert call(keep=ml2.ML2_MAX_TOPK + 1) == ml2.ML2_ERR_UNSUPPORTED
-    assert L.ml2_rerank(None, xp, 10, 8, P, 5, 3, P, P, P, P, s) == ml2.ML2_ERR_INVALID_ARG
+    assert L.ml2_rerank(None, xp, 10, 8, P, 5, 3, P, P, P, P, P, 1 << 20, s) == \
+        ml2.ML2_ERR_INVALID_ARG
+    with pytest.raises(ml2.Ml2Error) as ei:
+        ml2.ml2_rerank_workspace_bytes(a, -1)
+    assert ei.value.status == ml2.ML2_ERR_INVALID_ARG
+    with pytest.raises(ml2.Ml2Error) as ei:
+        ml2.ml2_rerank_workspace_bytes(a, ml2.ML2_MAX_TOPK + 1)
+    assert ei.value.status == ml2.ML2_ERR_UNSUPPORTED
+    assert ml2.ml2_rerank_workspace_bytes(a, 1000) >= 16 * 1000 * 4
     torch.cuda.synchronize()
     a.free()
