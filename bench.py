@@ -104,6 +104,48 @@ def cpu_baseline(w, rows: int):
                       f"({os.cpu_count()} visible cpus)"}
 
 
+def explore(args, w, X, v, p, dev) -> int:
+    """The explorer's rounds (Section 2; N = 10, alpha = 1 in Section 3): each
+    round holds (alpha+1)N accepted rows by P, model A keeps N.  Timed twice:
+    rescoring the pool every round (models retrained between rounds, as in
+    the paper) and reusing the scores (models unchanged)."""
+    import torch
+    from paper_2411_10764_amd import ml2
+    N = args.N
+    k = int(round((args.alpha + 1) * N))
+    a = ml2.ml2_load_ensemble(w.second_level()) if w.a_trees else None
+    R = args.explore
+    ex = ml2.Explorer(v, p, a, w.n, k, N, R)
+    idx = torch.empty(N, dtype=torch.int32, device=dev)
+    top = torch.empty(N, dtype=torch.float32, device=dev)
+    num = torch.empty(1, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream()
+    out = {"metric": "explorer rounds/sec", "unit": "rounds/s", "n_gpus": 1,
+           "higher_is_better": True, "dtype": "f32", "data": "synthetic",
+           "config": {"workload": w.name, "candidates": w.n, "N": N, "alpha": args.alpha,
+                      "held_per_round": k, "rounds": R,
+                      "second_level": f"{w.a_trees} trees x depth {w.a_depth}" if a else None}}
+    for mode, rescore in (("rescore", True), ("reuse", False)):
+        ex.reset()
+        ex.round(X, idx, top, num, rescore=True, stream=stream)  # warm, and scores for "reuse"
+        torch.cuda.synchronize()
+        ex.reset()
+        ex.round(X, idx, top, num, rescore=True, stream=stream)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(R - 1):
+            ex.round(X, idx, top, num, rescore=rescore, stream=stream)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        out[mode] = {"rounds_per_s": (R - 1) / dt, "ms_per_round": 1000 * dt / (R - 1),
+                     "proposed_last_round": int(num.item())}
+        _log(f"{mode}: {1000 * dt / (R - 1):.3f} ms per round over {R - 1} rounds")
+    out["value"] = out["rescore"]["rounds_per_s"]
+    ex.free()
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -113,6 +155,11 @@ def main() -> int:
     ap.add_argument("--cpu-rows", type=int, default=1 << 20)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-probe", action="store_true")
+    ap.add_argument("--explore", type=int, default=0, metavar="ROUNDS",
+                    help="time ROUNDS explorer rounds (N = --N proposed per round, "
+                         "(alpha+1)N held) instead of the scoring step")
+    ap.add_argument("--N", type=int, default=10)
+    ap.add_argument("--alpha", type=float, default=1.0)
     args = ap.parse_args()
 
     if args.copy_probe:
@@ -147,6 +194,8 @@ def main() -> int:
 
     v = ml2.ml2_load_ensemble(w.validity())
     p = ml2.ml2_load_ensemble(w.perf())
+    if args.explore:
+        return explore(args, w, X, v, p, dev)
     pipe = ml2.Pipeline(v, p, w.n, w.k, device=dev)
     second = w.a_trees > 0
     if second:  # model A re-ranks the k held configurations and keeps w.keep
