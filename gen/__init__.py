@@ -62,7 +62,13 @@ def _load():
         lib.ml2gen_features.restype = None
         lib.ml2gen_features.argtypes = [
             ctypes.c_uint64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
-            ctypes.c_int32, ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int32]
+            ctypes.c_int32, ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int32,
+            ctypes.c_double]
+        lib.ml2gen_ragged_trees.restype = ctypes.c_int64
+        lib.ml2gen_ragged_trees.argtypes = [
+            ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+            ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_int32, ctypes.c_int32,
+            ctypes.c_double] + [ctypes.c_void_p] * 7
         lib.ml2gen_perfect_trees.restype = None
         lib.ml2gen_perfect_trees.argtypes = [
             ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int32, ctypes.c_int32,
@@ -101,6 +107,9 @@ class Ensemble:
     feature: np.ndarray       # int32 [nodes]
     threshold: np.ndarray     # float32 [nodes]
     value: np.ndarray         # float32 [nodes] (leaves only)
+    # uint8 [nodes] or None: a missing (NaN) feature value goes left at an
+    # internal node with a nonzero entry, right otherwise (None: always right)
+    default_left: np.ndarray | None = None
 
     @property
     def num_trees(self) -> int:
@@ -128,13 +137,39 @@ def perfect_ensemble(seed: int, stream: int, trees: int, depth: int, F: int, K: 
     return Ensemble(F, float(np.float32(base_score)), off, left, right, feat, thr, val)
 
 
+def ragged_ensemble(seed: int, stream: int, trees: int, max_depth: int, F: int, K: int,
+                    leaf_sigma: float, base_score: float = 0.0, p_split: float = 0.9,
+                    decay: float = 0.9, p_left: float = 0.5,
+                    max_nodes: int = 2047) -> Ensemble:
+    """`trees` ragged trees of at most `max_depth` split levels with default
+    directions for missing values (see ml2gen.c)."""
+    cap = trees * max_nodes
+    off = np.empty(trees + 1, np.int64)
+    left = np.empty(cap, np.int32)
+    right = np.empty(cap, np.int32)
+    feat = np.empty(cap, np.int32)
+    thr = np.empty(cap, np.float32)
+    val = np.empty(cap, np.float32)
+    dl = np.empty(cap, np.uint8)
+    total = _load().ml2gen_ragged_trees(
+        seed, stream, trees, max_depth, max_nodes, float(p_split), float(decay),
+        float(p_left), F, K, float(leaf_sigma), off.ctypes.data, left.ctypes.data,
+        right.ctypes.data, feat.ctypes.data, thr.ctypes.data, val.ctypes.data, dl.ctypes.data)
+    if total < 0:
+        raise MemoryError("ragged tree generation failed")
+    return Ensemble(F, float(np.float32(base_score)), off, left[:total].copy(),
+                    right[:total].copy(), feat[:total].copy(), thr[:total].copy(),
+                    val[:total].copy(), dl[:total].copy())
+
+
 def features(seed: int, n: int, F: int, K: int, *, rows=None, row0: int = 0,
              ld: int | None = None, out: np.ndarray | None = None,
-             threads: int | None = None) -> np.ndarray:
+             threads: int | None = None, missing: float = 0.0) -> np.ndarray:
     """Rows of the seeded N x F candidate matrix as float32 [m, ld].
 
     With ``rows`` (int64 indices) the output holds those global rows in that
-    order; otherwise rows ``row0 .. row0+n-1``.
+    order; otherwise rows ``row0 .. row0+n-1``.  With ``missing`` > 0 each
+    hidden value is NaN (missing) with that probability.
     """
     ld = F if ld is None else ld
     if rows is not None:
@@ -147,7 +182,7 @@ def features(seed: int, n: int, F: int, K: int, *, rows=None, row0: int = 0,
     assert out.dtype == np.float32 and out.flags.c_contiguous and out.shape == (m, ld)
     _load().ml2gen_features(
         seed, rows.ctypes.data if rows is not None else None, row0, m, F, K, ld,
-        out.ctypes.data, threads or default_threads())
+        out.ctypes.data, threads or default_threads(), float(missing))
     return out
 
 

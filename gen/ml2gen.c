@@ -74,15 +74,24 @@ typedef struct {
   int32_t F, K;
   int64_t ld;
   float *X;
+  uint32_t missing_u24; /* hidden values are NaN with probability missing_u24 / 2^24 */
 } feat_job;
+
+#define STREAM_MISSING 4
 
 static void *feat_worker(void *p) {
   feat_job *j = (feat_job *)p;
   for (int64_t r = j->lo; r < j->hi; ++r) {
     int64_t row = j->rows ? j->rows[r] : j->row0 + r;
     float *dst = j->X + r * j->ld;
-    for (int32_t f = 0; f < j->F; ++f)
-      dst[f] = feature_value(j->seed, (uint64_t)row * (uint64_t)j->F + (uint64_t)f, f, j->K);
+    for (int32_t f = 0; f < j->F; ++f) {
+      const uint64_t ctr = (uint64_t)row * (uint64_t)j->F + (uint64_t)f;
+      if (f >= j->K && j->missing_u24 &&
+          u24(ml2gen_hash(j->seed, STREAM_MISSING, ctr)) < j->missing_u24)
+        dst[f] = NAN;
+      else
+        dst[f] = feature_value(j->seed, ctr, f, j->K);
+    }
   }
   return NULL;
 }
@@ -90,10 +99,16 @@ static void *feat_worker(void *p) {
 /*
  * Write m rows of the N x F feature matrix of `seed` into X (row stride ld
  * floats).  Row r of the output is global row rows[r], or row0 + r when rows
- * is NULL.  Columns F..ld-1 are left untouched.
+ * is NULL.  Columns F..ld-1 are left untouched.  With missing > 0 each hidden
+ * value (column >= K) is NaN -- a missing value -- with that probability
+ * (stream 4, one draw per element).
  */
 void ml2gen_features(uint64_t seed, const int64_t *rows, int64_t row0, int64_t m,
-                     int32_t F, int32_t K, int64_t ld, float *X, int32_t nthreads) {
+                     int32_t F, int32_t K, int64_t ld, float *X, int32_t nthreads,
+                     double missing) {
+  const uint32_t miss = missing <= 0.0 ? 0u
+                      : missing >= 1.0 ? (1u << 24)
+                                       : (uint32_t)(missing * 16777216.0);
   if (m <= 0) return;
   if (nthreads < 1) nthreads = 1;
   if (nthreads > 256) nthreads = 256;
@@ -110,6 +125,7 @@ void ml2gen_features(uint64_t seed, const int64_t *rows, int64_t row0, int64_t m
     jobs[t].K = K;
     jobs[t].ld = ld;
     jobs[t].X = X;
+    jobs[t].missing_u24 = miss;
   }
   for (int32_t t = 1; t < nthreads; ++t) pthread_create(&th[t], NULL, feat_worker, &jobs[t]);
   feat_worker(&jobs[0]);
@@ -161,4 +177,75 @@ void ml2gen_perfect_trees(uint64_t seed, uint64_t stream, int32_t T, int32_t dep
       }
     }
   }
+}
+
+/*
+ * T ragged trees grown breadth-first (the shape of XGBoost trees trained to a
+ * maximum depth): the root splits, a node at depth d in 1..max_depth-1 splits
+ * with probability p_split * decay^(d-1), a node at max_depth is a leaf, and a
+ * split that would take the tree past max_nodes nodes becomes a leaf.  Node
+ * ids are breadth-first (the children of a node are adjacent, left first).
+ * Split features are uniform over 0..F-1 with thresholds from the feature's
+ * own distribution, as for perfect trees; default_left is 1 with probability
+ * p_left on internal nodes.  Per node i of tree t the draws use counters
+ * 8*c + {0: feature, 1: knob threshold, 2-3: lognormal threshold, 4: split,
+ * 5: default direction, 6-7: leaf}, c = (t << 32) + i.  Arrays hold room
+ * for T * max_nodes nodes; returns the number of nodes written.
+ */
+int64_t ml2gen_ragged_trees(uint64_t seed, uint64_t stream, int32_t T, int32_t max_depth,
+                            int32_t max_nodes, double p_split, double decay, double p_left,
+                            int32_t F, int32_t K, double leaf_sigma, int64_t *off,
+                            int32_t *left, int32_t *right, int32_t *feat, float *thr,
+                            float *leaf, uint8_t *dleft) {
+  int32_t *depth = (int32_t *)malloc((size_t)(max_nodes > 0 ? max_nodes : 1) * sizeof(int32_t));
+  if (!depth) return -1;
+  int64_t g0 = 0;
+  for (int32_t t = 0; t < T; ++t) {
+    off[t] = g0;
+    int32_t count = 1;
+    depth[0] = 0;
+    for (int32_t i = 0; i < count; ++i) {
+      const int64_t g = g0 + i;
+      const uint64_t c = ((uint64_t)t << 32) + (uint64_t)i;
+      const int32_t d = depth[i];
+      int split = 0;
+      if (d == 0) {
+        split = max_depth > 0;
+      } else if (d < max_depth) {
+        const double p = p_split * pow(decay, (double)(d - 1));
+        split = (double)u24(ml2gen_hash(seed, stream, 8 * c + 4)) < p * 16777216.0;
+      }
+      if (split && count + 2 > max_nodes) split = 0;
+      if (split) {
+        const int32_t f = index_of(ml2gen_hash(seed, stream, 8 * c), F);
+        float th;
+        if (f < K)
+          th = (float)knob_of(ml2gen_hash(seed, stream, 8 * c + 1));
+        else
+          th = (float)exp(normal_of(ml2gen_hash(seed, stream, 8 * c + 2),
+                                    ml2gen_hash(seed, stream, 8 * c + 3)));
+        left[g] = count;
+        right[g] = count + 1;
+        feat[g] = f;
+        thr[g] = th;
+        leaf[g] = 0.0f;
+        dleft[g] = (double)u24(ml2gen_hash(seed, stream, 8 * c + 5)) < p_left * 16777216.0;
+        depth[count] = d + 1;
+        depth[count + 1] = d + 1;
+        count += 2;
+      } else {
+        left[g] = -1;
+        right[g] = -1;
+        feat[g] = -1;
+        thr[g] = 0.0f;
+        dleft[g] = 0;
+        leaf[g] = (float)(leaf_sigma * normal_of(ml2gen_hash(seed, stream, 8 * c + 6),
+                                                  ml2gen_hash(seed, stream, 8 * c + 7)));
+      }
+    }
+    g0 += count;
+  }
+  off[T] = g0;
+  free(depth);
+  return g0;
 }

@@ -12,7 +12,9 @@
  *
  * Conventions shared by every call:
  *   - A split sends a candidate LEFT iff x[feature] < threshold (XGBoost's
- *     rule): a tie or a NaN feature goes right.
+ *     rule): a tie goes right.  A NaN feature is a missing value and takes
+ *     the node's default direction (XGBoost's missing-value rule): left
+ *     where the ensemble's default_left is set, right otherwise.
  *   - A margin is base_score + leaf(tree 0) + leaf(tree 1) + ... computed in
  *     float32 as a left fold in tree-index order, round-to-nearest-even, no
  *     fused operations, subnormals kept.  Results are bit-identical to that
@@ -49,7 +51,8 @@ typedef enum {
 } ml2_status;
 
 /* Library limits (checked at load / call time, ML2_ERR_UNSUPPORTED beyond). */
-#define ML2_MAX_DEPTH 12        /* longest root-to-leaf path, in splits */
+#define ML2_MAX_DEPTH 32        /* longest root-to-leaf path, in splits */
+#define ML2_MAX_TREE_NODES 2041 /* nodes of one tree in the ragged layout */
 #define ML2_MAX_FEATURES 256    /* num_features of an ensemble */
 #define ML2_MAX_TOPK 16384      /* k of ml2_filter_topk; m and keep of ml2_rerank */
 
@@ -69,10 +72,18 @@ typedef struct ml2_ensemble ml2_ensemble; /* opaque; immutable after load */
  *   split_feature, split_threshold  internal nodes only (threshold not NaN;
  *                   +-inf allowed)
  *   leaf_value      leaves only; finite
+ *   default_left    NULL, or per node: nonzero sends a missing (NaN) feature
+ *                   value left at that internal node (ignored on leaves);
+ *                   with NULL every missing value goes right
  * Every node of a tree must be reachable from its root exactly once (no
  * cycles, no shared or orphan nodes), and no root-to-leaf path may have more
  * than ML2_MAX_DEPTH splits.  The sum T * max|leaf| + |base_score| must stay
  * below FLT_MAX / 2 so that no partial sum overflows.
+ * Device layouts: ensembles whose paths have at most 12 splits and no
+ * default-left node are padded to perfect trees unless that is more than
+ * four times their node count; the others are packed tree by tree into
+ * 24 KiB chunks, which holds trees of at most ML2_MAX_TREE_NODES nodes
+ * (Table 3's depth-14 models trained on the paper's data are far smaller).
  */
 typedef struct {
   int32_t num_trees;
@@ -84,6 +95,7 @@ typedef struct {
   const int32_t *split_feature;
   const float *split_threshold;
   const float *leaf_value;
+  const uint8_t *default_left;
 } ml2_ensemble_desc;
 
 /*
@@ -92,8 +104,8 @@ typedef struct {
  * way.  On success *out owns its device tables until ml2_free_ensemble; a
  * loaded ensemble may be used from several threads and streams at once.
  * Errors: INVALID_ARG (NULL pointers, malformed trees, out-of-range feature,
- * NaN threshold, non-finite leaf, overflow bound), UNSUPPORTED (depth or F
- * beyond the limits), OUT_OF_MEMORY, HIP.  *out is set to NULL on error.
+ * NaN threshold, non-finite leaf, overflow bound), UNSUPPORTED (depth, F or
+ * tree size beyond the limits), OUT_OF_MEMORY, HIP.  *out is set to NULL on error.
  */
 ml2_status ml2_load_ensemble(const ml2_ensemble_desc *desc, ml2_ensemble **out);
 
@@ -101,7 +113,8 @@ ml2_status ml2_load_ensemble(const ml2_ensemble_desc *desc, ml2_ensemble **out);
  * no work that uses it may still be pending. */
 void ml2_free_ensemble(ml2_ensemble *e);
 
-/* Number of features / trees / padded depth of a loaded ensemble (-1 on NULL). */
+/* Number of features / trees / depth (the longest path, or the padded depth
+ * of the perfect layout) of a loaded ensemble (-1 on NULL). */
 int32_t ml2_ensemble_num_features(const ml2_ensemble *e);
 int32_t ml2_ensemble_num_trees(const ml2_ensemble *e);
 int32_t ml2_ensemble_depth(const ml2_ensemble *e);

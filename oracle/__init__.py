@@ -43,6 +43,7 @@ class _Ens(ctypes.Structure):
         ("feature", ctypes.c_void_p),
         ("threshold", ctypes.c_void_p),
         ("value", ctypes.c_void_p),
+        ("default_left", ctypes.c_void_p),
     ]
 
 
@@ -87,12 +88,15 @@ class OracleEnsemble:
             np.ascontiguousarray(ens.threshold, np.float32),
             np.ascontiguousarray(ens.value, np.float32),
         )
+        dl = getattr(ens, "default_left", None)
+        self.dl = None if dl is None else np.ascontiguousarray(dl, np.uint8)
         off, left, right, feat, thr, val = self.arrays
         self.num_trees = int(off.shape[0] - 1)
         self.num_features = int(ens.num_features)
         self.s = _Ens(self.num_trees, self.num_features, float(ens.base_score),
                       off.ctypes.data, left.ctypes.data, right.ctypes.data,
-                      feat.ctypes.data, thr.ctypes.data, val.ctypes.data)
+                      feat.ctypes.data, thr.ctypes.data, val.ctypes.data,
+                      None if self.dl is None else self.dl.ctypes.data)
 
     @property
     def ptr(self):

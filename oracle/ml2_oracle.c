@@ -24,7 +24,9 @@
  *
  * Readings taken where the paper is silent:
  *   - a split sends x LEFT iff x[feature] < threshold (XGBoost's rule), so a
- *     tie or a NaN feature goes right;
+ *     tie goes right; a missing (NaN) feature takes the node's default
+ *     direction, left where default_left is set, right otherwise (XGBoost's
+ *     missing-value rule; without default_left every NaN goes right);
  *   - the margin is base_score + leaf_0 + leaf_1 + ... summed in float32, left
  *     to right in tree-index order, round-to-nearest-even, no fused operations,
  *     subnormals kept;
@@ -50,6 +52,7 @@ typedef struct {
   const int32_t *feature;
   const float *threshold;
   const float *value;       /* leaf values */
+  const uint8_t *default_left; /* NULL, or nonzero: a NaN feature goes left */
 } ml2o_ensemble;
 
 /* Leaf value tree t assigns to the feature vector x.  Returns NaN if the tree
@@ -63,7 +66,10 @@ float ml2o_tree_leaf(const ml2o_ensemble *e, int32_t t, const float *x) {
     int32_t r = e->right[base + node];
     if (l < 0 && r < 0) return e->value[base + node];
     float xv = x[e->feature[base + node]];
-    node = (xv < e->threshold[base + node]) ? l : r;
+    if (isnan(xv))
+      node = (e->default_left && e->default_left[base + node]) ? l : r;
+    else
+      node = (xv < e->threshold[base + node]) ? l : r;
   }
   return NAN;
 }

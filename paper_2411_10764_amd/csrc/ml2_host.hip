@@ -6,6 +6,7 @@
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <mutex>
@@ -84,6 +85,7 @@ ml2_status current_device(int *dev) {
 struct TreeView {
   const int32_t *left, *right, *feat;
   const float *thr, *val;
+  const uint8_t *dl;  // NULL: every missing value goes right
   int64_t size;
 };
 
@@ -169,6 +171,102 @@ void pad_tree(const TreeView &tv, int D, char *rec) {
   }
 }
 
+// ---- ragged layout ---------------------------------------------------------
+
+// Pack trees (breadth-first renumbered: siblings adjacent) into fixed chunk
+// slots (format in ml2_internal.h).  Returns the number of slots and the
+// total tree count with the padding trees.
+struct RaggedPack {
+  std::vector<char> bytes;
+  int32_t slots = 0;
+  int32_t trees = 0;
+  int32_t depth = 0;
+};
+
+void pack_ragged(const std::vector<TreeView> &views, const std::vector<int> &depths,
+                 RaggedPack *out) {
+  constexpr uint32_t CAP = ml2::kRaggedChunkBytes;
+  constexpr int GRP = ml2::kRaggedGroup;
+  const uint32_t leaf_word0 = (uint32_t)(-8) << 9;  // offset -8: the node itself
+  const uint32_t nan_bits = 0x7FC00000u;
+  size_t t = 0;
+  int32_t tree_index = 0;
+  while (t < views.size()) {
+    // choose the trees of this slot: header + roots + 12 bytes per node,
+    // with room left for padding the tree count to a multiple of GRP
+    size_t first = t, nodes = 0;
+    auto need = [&](size_t ntrees, size_t nnodes) {
+      const size_t ntr = (ntrees + GRP - 1) / GRP * GRP;
+      const size_t head = (16 + 4 * ntr + 15) & ~(size_t)15;
+      return head + 12 * (nnodes + (ntr - ntrees));
+    };
+    while (t < views.size() && need(t + 1 - first, nodes + (size_t)views[t].size) <= CAP) {
+      nodes += (size_t)views[t].size;
+      ++t;
+    }
+    const size_t real = t - first;
+    const size_t ntr = (real + GRP - 1) / GRP * GRP;
+    const size_t all_nodes = nodes + (ntr - real);
+    const uint32_t head = (uint32_t)((16 + 4 * ntr + 15) & ~(size_t)15);
+    const uint32_t vals = head + 8u * (uint32_t)all_nodes;
+    const size_t slot0 = out->bytes.size();
+    out->bytes.resize(slot0 + CAP, 0);
+    char *slot = out->bytes.data() + slot0;
+    uint32_t *root = reinterpret_cast<uint32_t *>(slot + 16);
+    uint2 *node = reinterpret_cast<uint2 *>(slot + head);
+    float *val = reinterpret_cast<float *>(slot + vals);
+    int depth = 0;
+    uint32_t next = 0;  // next free node index in the slot
+    std::vector<int32_t> order;
+    for (size_t i = 0; i < ntr; ++i) {
+      root[i] = head + 8u * next;
+      if (i >= real) {  // padding: one leaf of value -0.0
+        node[next] = make_uint2(leaf_word0, nan_bits);
+        val[next] = -0.0f;
+        ++next;
+        continue;
+      }
+      const TreeView &tv = views[first + i];
+      if (depths[first + i] > depth) depth = depths[first + i];
+      // breadth-first ids: order[k] = original node of new id k
+      order.assign(1, 0);
+      std::vector<int32_t> newid((size_t)tv.size, -1);
+      newid[0] = 0;
+      for (size_t k = 0; k < order.size(); ++k) {
+        const int32_t o = order[k];
+        if (tv.left[o] == -1) continue;
+        newid[(size_t)tv.left[o]] = (int32_t)order.size();
+        order.push_back(tv.left[o]);
+        newid[(size_t)tv.right[o]] = (int32_t)order.size();
+        order.push_back(tv.right[o]);
+      }
+      for (size_t k = 0; k < order.size(); ++k) {
+        const int32_t o = order[k];
+        const uint32_t j = next + (uint32_t)k;
+        if (tv.left[o] == -1) {
+          node[j] = make_uint2(leaf_word0, nan_bits);
+          val[j] = tv.val[o];
+        } else {
+          const int32_t rel = 8 * (newid[(size_t)tv.left[o]] - (int32_t)k);
+          const uint32_t dl = (tv.dl && tv.dl[o]) ? 1u : 0u;
+          uint32_t tb;
+          memcpy(&tb, &tv.thr[o], 4);
+          node[j] = make_uint2(((uint32_t)rel << 9) | (dl << 8) | (uint32_t)tv.feat[o], tb);
+          val[j] = 0.0f;
+        }
+      }
+      next += (uint32_t)order.size();
+    }
+    // values are addressed as vbias + (node byte offset) / 2
+    const uint32_t hdr[4] = {(uint32_t)ntr, (uint32_t)depth, vals - head / 2, (uint32_t)tree_index};
+    memcpy(slot, hdr, sizeof hdr);
+    tree_index += (int32_t)ntr;
+    if (depth > out->depth) out->depth = depth;
+    out->slots += 1;
+  }
+  out->trees = tree_index;
+}
+
 void pad_identity_tree(int D, char *rec) {  // every leaf -0.0
   const uint32_t L = 1u << D;
   float *leaves = reinterpret_cast<float *>(rec + 4u * L);
@@ -218,45 +316,92 @@ ml2_status ml2_load_ensemble(const ml2_ensemble_desc *desc, ml2_ensemble **out) 
                 (long long)d.tree_node_offset[0]);
   int depth = 1;
   double max_leaf = 0.0;
+  int64_t total_nodes = 0, max_nodes = 0;
+  bool any_default_left = false;
   std::vector<TreeView> views((size_t)d.num_trees);
+  std::vector<int> depths((size_t)d.num_trees);
   for (int32_t t = 0; t < d.num_trees; ++t) {
     const int64_t a = d.tree_node_offset[t], b = d.tree_node_offset[t + 1];
     if (b <= a || b - a > (int64_t)INT32_MAX)
       return fail(ML2_ERR_INVALID_ARG, "tree %d: node range [%lld, %lld) is empty or too large",
                   t, (long long)a, (long long)b);
     TreeView tv{d.left_child + a, d.right_child + a, d.split_feature + a,
-                d.split_threshold + a, d.leaf_value + a, b - a};
+                d.split_threshold + a, d.leaf_value + a,
+                d.default_left ? d.default_left + a : nullptr, b - a};
     int dt = 0;
     ml2_status st = check_tree(d, t, tv, &dt, &max_leaf);
     if (st != ML2_OK) return st;
     if (dt > depth) depth = dt;
+    depths[(size_t)t] = dt;
     views[(size_t)t] = tv;
+    total_nodes += tv.size;
+    if (tv.size > max_nodes) max_nodes = tv.size;
+    if (tv.dl)
+      for (int64_t i = 0; i < tv.size && !any_default_left; ++i)
+        any_default_left = tv.left[i] != -1 && tv.dl[i] != 0;
   }
   if ((double)d.num_trees * max_leaf + fabs((double)d.base_score) >= (double)FLT_MAX / 2)
     return fail(ML2_ERR_INVALID_ARG, "num_trees * max|leaf| + |base| may overflow float32");
+
+  // Layout: perfect padded trees where they represent the ensemble and are
+  // not much larger than its nodes; ragged slots otherwise (deeper than the
+  // perfect limit, default directions, or sparse trees).  ML2_LAYOUT=ragged
+  // or =perfect forces a layout that can represent the ensemble.
+  const int64_t tpad16 = (d.num_trees + ml2::kTreePad - 1) / ml2::kTreePad * ml2::kTreePad;
+  const bool perfect_ok = depth <= ml2::kMaxPerfectDepth && !any_default_left;
+  const bool ragged_ok = max_nodes <= ML2_MAX_TREE_NODES;
+  bool ragged = !perfect_ok ||
+                (ragged_ok && (double)tpad16 * ml2::record_bytes(depth) > 4.0 * 12.0 * total_nodes);
+  if (const char *lay = getenv("ML2_LAYOUT")) {
+    if (!strcmp(lay, "ragged") && ragged_ok) ragged = true;
+    if (!strcmp(lay, "perfect") && perfect_ok) ragged = false;
+  }
+  if (ragged && !ragged_ok)
+    return fail(ML2_ERR_UNSUPPORTED,
+                "a tree of %lld nodes needs the ragged layout (deeper than %d levels or default "
+                "directions), which holds at most %d nodes per tree",
+                (long long)max_nodes, ml2::kMaxPerfectDepth, ML2_MAX_TREE_NODES);
 
   ml2::Forest f{};
   ml2_status st = current_device(&f.device);
   if (st != ML2_OK) return st;
   f.num_trees = d.num_trees;
-  f.num_trees_padded = (d.num_trees + ml2::kTreePad - 1) / ml2::kTreePad * ml2::kTreePad;
   f.num_features = d.num_features;
-  f.depth = depth;
   f.base = d.base_score;
-  f.rec_bytes = ml2::record_bytes(depth);
-  const size_t bytes = (size_t)f.num_trees_padded * f.rec_bytes;
+  f.ragged = ragged ? 1 : 0;
   std::vector<char> host;
-  try {
-    host.assign(bytes, 0);
-  } catch (const std::bad_alloc &) {
-    return fail(ML2_ERR_OUT_OF_MEMORY, "host staging of %zu bytes failed", bytes);
-  }
-  for (int32_t t = 0; t < f.num_trees_padded; ++t) {
-    char *rec = host.data() + (size_t)t * f.rec_bytes;
-    if (t < d.num_trees)
-      pad_tree(views[(size_t)t], depth, rec);
-    else
-      pad_identity_tree(depth, rec);
+  size_t bytes = 0;
+  if (ragged) {
+    RaggedPack pk;
+    try {
+      pack_ragged(views, depths, &pk);
+    } catch (const std::bad_alloc &) {
+      return fail(ML2_ERR_OUT_OF_MEMORY, "host staging of the ragged layout failed");
+    }
+    f.num_trees_padded = pk.trees;
+    f.records = pk.slots;
+    f.depth = pk.depth;
+    f.rec_bytes = ml2::record_bytes(0);
+    host.swap(pk.bytes);
+    bytes = host.size();
+  } else {
+    f.num_trees_padded = (int32_t)tpad16;
+    f.records = f.num_trees_padded;
+    f.depth = depth;
+    f.rec_bytes = ml2::record_bytes(depth);
+    bytes = (size_t)f.num_trees_padded * f.rec_bytes;
+    try {
+      host.assign(bytes, 0);
+    } catch (const std::bad_alloc &) {
+      return fail(ML2_ERR_OUT_OF_MEMORY, "host staging of %zu bytes failed", bytes);
+    }
+    for (int32_t t = 0; t < f.num_trees_padded; ++t) {
+      char *rec = host.data() + (size_t)t * f.rec_bytes;
+      if (t < d.num_trees)
+        pad_tree(views[(size_t)t], depth, rec);
+      else
+        pad_identity_tree(depth, rec);
+    }
   }
   // The tree table is followed by kTreeSlack zero bytes: chunk staging reads
   // whole register sets, past the end of the last chunk.

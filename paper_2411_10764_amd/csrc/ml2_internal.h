@@ -24,9 +24,31 @@ namespace ml2 {
 // taken otherwise, so a walk moves with u <- 2u + [x < t].  Byte 0..7 is
 // unused.
 constexpr int kTreePad = 16;  // >= the trees of the largest walk group
+constexpr int kMaxPerfectDepth = 12;  // deeper ensembles use the ragged layout
+
+// Ragged layout (deep or sparse trees, or per-node default directions for
+// missing values): the ensemble is cut into chunks of whole trees, each in a
+// fixed slot of kRaggedChunkBytes bytes:
+//   byte 0   uint4 {trees in the chunk (a multiple of kRaggedGroup), deepest
+//            path of those trees, vbias, global index of the chunk's first
+//            tree}; the value of the node at byte offset u is at vbias + u/2
+//   byte 16  uint32 root byte offset of each tree (from the slot start)
+//   then 8-byte nodes, each tree breadth-first (siblings adjacent):
+//     word 0: bits 31..9 signed byte offset from the node to its left child
+//             (the right child follows it), bit 8 default-left, bits 7..0
+//             split feature; word 1: threshold bits
+//     a leaf steps back onto itself: offset -8, threshold NaN, so x < t is
+//     false, it "goes right" to itself and a lockstep walk may run past it
+//   then one float per node (the leaf values; 0 for splits)
+// Trees padded onto a chunk are single leaves of value -0.0.
+constexpr uint32_t kRaggedChunkBytes = 24 * 1024;
+constexpr int kRaggedGroup = 4;
 constexpr size_t kTreeSlack = 128 * 1024;  // readable zero bytes after the tree table
 
+// Bytes of one staged record: a perfect tree of `depth` levels, or (depth 0)
+// one ragged chunk slot.
 inline constexpr uint32_t record_bytes(int depth) {
+  if (depth == 0) return kRaggedChunkBytes;
   const uint32_t raw = 12u << depth;
   return (raw + 15u) & ~15u;
 }
@@ -34,12 +56,14 @@ inline constexpr uint32_t record_bytes(int depth) {
 struct Forest {
   int device;
   int32_t num_trees;        // trees in the descriptor
-  int32_t num_trees_padded; // multiple of kTreePad
+  int32_t num_trees_padded; // with the padding trees (perfect: a multiple of kTreePad)
   int32_t num_features;
-  int32_t depth;            // D >= 1
+  int32_t depth;            // deepest path (perfect: the padded depth, >= 1)
+  int32_t ragged;           // 1: ragged layout
+  int32_t records;          // staged records: perfect trees, or ragged chunk slots
   float base;
-  uint32_t rec_bytes;
-  void *d_trees;            // num_trees_padded * rec_bytes bytes
+  uint32_t rec_bytes;       // record_bytes(depth), or record_bytes(0) when ragged
+  void *d_trees;            // records * rec_bytes bytes (+ kTreeSlack zero bytes)
 };
 
 // Launch parameters of a walk (chosen on the host from D and F).

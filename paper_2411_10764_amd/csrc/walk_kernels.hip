@@ -81,7 +81,8 @@ struct WalkArgs {
   const uint8_t *valid_in;  // perf
   float *score_out;         // perf; the fold of a row list
   const int32_t *rows_in;   // row list: entry i is pool row rows_in[i]
-  float *leaves_out;        // leaf walk of a row list: [ntrees][n]
+  float *leaves_out;        // leaf walk of a row list: [fold_trees][n]
+  int32_t fold_trees;       // trees (with padding trees) the fold adds up
 };
 
 // Row `row` of X into the tile of its candidate (dst = tile + 4*candidate),
@@ -305,6 +306,112 @@ struct Walks {
   }
 };
 
+// H walks of one half over a ragged chunk slot: u is the byte offset of the
+// current node in the slot.  One step: x < t goes left, a missing x goes
+// left where the node's default is left, else right; the right child follows
+// the left one, and a leaf steps onto itself.
+template <int H, int S>
+struct RWalks {
+  uint32_t u[H];
+  uint2 nd[H];
+  float x[H];
+  float leaf[H];
+
+  __device__ __forceinline__ void read_nodes(const char *slot) {
+#pragma unroll
+    for (int g = 0; g < H; ++g) nd[g] = *reinterpret_cast<const uint2 *>(slot + u[g]);
+  }
+  __device__ __forceinline__ void read_features(const char *tile_lane) {
+#pragma unroll
+    for (int g = 0; g < H; ++g)
+      x[g] = *reinterpret_cast<const float *>(tile_lane + ((nd[g].x & 0xFFu) << Geo<S>::kRowShift));
+  }
+  __device__ __forceinline__ void descend() {
+#pragma unroll
+    for (int g = 0; g < H; ++g) {
+      const float t = __uint_as_float(nd[g].y);
+      const bool left = (x[g] < t) || ((nd[g].x & 0x100u) != 0u && __builtin_isnan(x[g]));
+      u[g] = u[g] + (uint32_t)((int32_t)nd[g].x >> 9) + (left ? 0u : 8u);
+    }
+  }
+  __device__ __forceinline__ void read_leaves(const char *slot, uint32_t vbias) {
+#pragma unroll
+    for (int g = 0; g < H; ++g)
+      leaf[g] = *reinterpret_cast<const float *>(slot + vbias + (u[g] >> 1));
+  }
+  __device__ __forceinline__ float fold(float m) const {
+#pragma unroll
+    for (int g = 0; g < H; ++g) m = m + leaf[g];
+    return m;
+  }
+  __device__ __forceinline__ float fold_upper(float m) const {
+#pragma unroll
+    for (int g = 0; g < H; ++g) m = m + from_upper_half(leaf[g]);
+    return m;
+  }
+};
+
+// Ragged chunk slot header (see ml2_internal.h), read from LDS into scalars.
+struct SlotHead {
+  int ntrees;
+  int depth;
+  uint32_t vbias;
+  int tree0;
+};
+
+__device__ __forceinline__ SlotHead slot_head(const char *slot) {
+  const uint4 h = *reinterpret_cast<const uint4 *>(slot);
+  return {__builtin_amdgcn_readfirstlane((int)h.x), __builtin_amdgcn_readfirstlane((int)h.y),
+          (uint32_t)__builtin_amdgcn_readfirstlane((int)h.z),
+          __builtin_amdgcn_readfirstlane((int)h.w)};
+}
+
+// One group of a ragged slot: the G trees whose root offsets start at
+// `roots` (in LDS), walked `depth` steps (the slot's deepest path).
+template <int G, int S, typename Done>
+__device__ __forceinline__ void walk_group_ragged(const char *slot, const uint32_t *roots,
+                                                  int depth, uint32_t vbias,
+                                                  const char *tile_lane, Done done) {
+  if constexpr (G == 1) {
+    RWalks<1, S> A;
+    A.u[0] = roots[0];
+    A.read_nodes(slot);
+    for (int l = 0; l < depth; ++l) {
+      A.read_features(tile_lane);
+      A.descend();
+      A.read_nodes(slot);
+    }
+    A.read_leaves(slot, vbias);
+    done(A, A);
+  } else {
+    constexpr int H = G / 2;
+    RWalks<H, S> A, B;
+#pragma unroll
+    for (int g = 0; g < H; ++g) {
+      A.u[g] = roots[g];
+      B.u[g] = roots[H + g];
+    }
+    A.read_nodes(slot);
+    B.read_nodes(slot);
+    __builtin_amdgcn_sched_barrier(0);
+    for (int l = 0; l < depth; ++l) {
+      A.read_features(tile_lane);
+      __builtin_amdgcn_sched_barrier(0);
+      B.read_features(tile_lane);
+      __builtin_amdgcn_sched_barrier(0);
+      A.descend();
+      A.read_nodes(slot);
+      __builtin_amdgcn_sched_barrier(0);
+      B.descend();
+      B.read_nodes(slot);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    A.read_leaves(slot, vbias);
+    B.read_leaves(slot, vbias);
+    done(A, B);
+  }
+}
+
 // One group: half-wave h walks the G trees of records starting at `rec`
 // (two halves of H = G/2 offset by half a level), then `done(A, B)` gets the
 // leaves (A: the first H trees, B: the next H; with G == 1 only A).
@@ -358,17 +465,26 @@ __device__ __forceinline__ float walk_chunk(const char *cb, int ntr, const char 
                                             int h, float m) {
   constexpr uint32_t RB = record_bytes(D);
   constexpr int GS = G * S;
-  for (int t0 = 0; t0 < ntr; t0 += GS) {
-    walk_group<D, G, S>(cb + (uint32_t)(t0 + h * G) * RB, tile_lane,
-                        [&](const auto &A, const auto &B) {
-                          if constexpr (G == 1) {
-                            m = A.fold(m);
-                            if constexpr (S == 2) m = A.fold_upper(m);
-                          } else {
-                            m = B.fold(A.fold(m));
-                            if constexpr (S == 2) m = B.fold_upper(A.fold_upper(m));
-                          }
-                        });
+  auto fold = [&](const auto &A, const auto &B) {
+    if constexpr (G == 1) {
+      m = A.fold(m);
+      if constexpr (S == 2) m = A.fold_upper(m);
+    } else {
+      m = B.fold(A.fold(m));
+      if constexpr (S == 2) m = B.fold_upper(A.fold_upper(m));
+    }
+  };
+  if constexpr (D == 0) {  // ntr ragged slots
+    for (int i = 0; i < ntr; ++i) {
+      const char *slot = cb + (uint32_t)i * RB;
+      const SlotHead hd = slot_head(slot);
+      const uint32_t *roots = reinterpret_cast<const uint32_t *>(slot + 16) + h * G;
+      for (int t0 = 0; t0 < hd.ntrees; t0 += GS)
+        walk_group_ragged<G, S>(slot, roots + t0, hd.depth, hd.vbias, tile_lane, fold);
+    }
+  } else {
+    for (int t0 = 0; t0 < ntr; t0 += GS)
+      walk_group<D, G, S>(cb + (uint32_t)(t0 + h * G) * RB, tile_lane, fold);
   }
   return m;
 }
@@ -606,10 +722,10 @@ __global__ void __launch_bounds__(kLanes * 4) leaves_kernel(WalkArgs a) {
   const int W = a.nthreads / kLanes;
   const size_t tile_bytes = (size_t)a.F * Geo<1>::kRowBytes;
   char *chunk = smem + W * tile_bytes;
-  const int t0 = blockIdx.x * a.chunk_trees;
-  const int nt = min(a.chunk_trees, a.ntrees - t0);  // a multiple of G
-  const u32x4 *src = reinterpret_cast<const u32x4 *>(a.trees + (size_t)t0 * RB);
-  for (uint32_t i = threadIdx.x; i < (uint32_t)nt * (RB / 16u); i += a.nthreads)
+  const int r0 = blockIdx.x * a.chunk_trees;         // first record
+  const int nr = min(a.chunk_trees, a.ntrees - r0);  // records (a multiple of G if perfect)
+  const u32x4 *src = reinterpret_cast<const u32x4 *>(a.trees + (size_t)r0 * RB);
+  for (uint32_t i = threadIdx.x; i < (uint32_t)nr * (RB / 16u); i += a.nthreads)
     reinterpret_cast<u32x4 *>(chunk)[i] = src[i];
   const int64_t pos = ((int64_t)blockIdx.y * W + wave) * kLanes + lane;
   int64_t row = -1;
@@ -620,18 +736,31 @@ __global__ void __launch_bounds__(kLanes * 4) leaves_kernel(WalkArgs a) {
   char *tile_lane = smem + wave * tile_bytes + 4 * lane;
   if (row >= 0) load_row<1>(a, row, tile_lane);
   __syncthreads();
-  for (int g0 = 0; g0 < nt; g0 += G) {
-    walk_group<D, G, 1>(chunk + (uint32_t)g0 * RB, tile_lane, [&](const auto &A, const auto &B) {
-      if (row < 0) return;
-      float *out = a.leaves_out + (size_t)(t0 + g0) * a.n + pos;
-      constexpr int H = G == 1 ? 1 : G / 2;
+  // the leaves of trees t .. t+G-1 of the ensemble
+  auto store = [&](int t, const auto &A, const auto &B) {
+    if (row < 0) return;
+    float *out = a.leaves_out + (size_t)t * a.n + pos;
+    constexpr int H = G == 1 ? 1 : G / 2;
 #pragma unroll
-      for (int g = 0; g < H; ++g) out[(size_t)g * a.n] = A.leaf[g];
-      if constexpr (G > 1) {
+    for (int g = 0; g < H; ++g) out[(size_t)g * a.n] = A.leaf[g];
+    if constexpr (G > 1) {
 #pragma unroll
-        for (int g = 0; g < H; ++g) out[(size_t)(H + g) * a.n] = B.leaf[g];
-      }
-    });
+      for (int g = 0; g < H; ++g) out[(size_t)(H + g) * a.n] = B.leaf[g];
+    }
+  };
+  if constexpr (D == 0) {
+    for (int i = 0; i < nr; ++i) {
+      const char *slot = chunk + (uint32_t)i * RB;
+      const SlotHead hd = slot_head(slot);
+      const uint32_t *roots = reinterpret_cast<const uint32_t *>(slot + 16);
+      for (int g0 = 0; g0 < hd.ntrees; g0 += G)
+        walk_group_ragged<G, 1>(slot, roots + g0, hd.depth, hd.vbias, tile_lane,
+                                [&](const auto &A, const auto &B) { store(hd.tree0 + g0, A, B); });
+    }
+  } else {
+    for (int g0 = 0; g0 < nr; g0 += G)
+      walk_group<D, G, 1>(chunk + (uint32_t)g0 * RB, tile_lane,
+                          [&](const auto &A, const auto &B) { store(r0 + g0, A, B); });
   }
 }
 
@@ -646,7 +775,7 @@ __global__ void __launch_bounds__(256) fold_kernel(WalkArgs a) {
     return;
   }
   float m = a.base;
-  for (int t = 0; t < a.ntrees; ++t) m = m + a.leaves_out[(size_t)t * a.n + i];
+  for (int t = 0; t < a.fold_trees; ++t) m = m + a.leaves_out[(size_t)t * a.n + i];
   a.score_out[i] = m;
 }
 
@@ -654,6 +783,7 @@ __global__ void __launch_bounds__(256) fold_kernel(WalkArgs a) {
 // must hold at least G whole trees.  S = 2: a 24 KiB register-staged chunk
 // must hold the 2G trees of a group.
 constexpr bool group_allowed(int d, int g, int s) {
+  if (d == 0) return kRaggedGroup % (g * s) == 0 && g <= 4;  // ragged slots
   if (s == 2)
     return d <= 7 ? (g == 4 || g == 8)
          : d == 8 ? (g == 2 || g == 4)
@@ -670,7 +800,8 @@ template <int D, int G, int S>
 hipError_t launch_dgs(bool perf, const WalkPlan &p, const WalkArgs &a, hipStream_t s) {
   // Chunks hold whole groups: every chunk's tree count, including the last
   // one's, is a multiple of the padding and hence of the group.
-  static_assert(kTreePad % (G * S) == 0, "a walk group must divide the tree padding");
+  static_assert((D == 0 ? kRaggedGroup : kTreePad) % (G * S) == 0,
+                "a walk group must divide the tree padding");
   const void *fn = perf ? reinterpret_cast<const void *>(&perf_kernel<D, G, S>)
                         : reinterpret_cast<const void *>(&validity_kernel<D, G, S>);
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -700,7 +831,7 @@ hipError_t launch_ds(bool perf, const WalkPlan &p, const WalkArgs &a, hipStream_
 template <int D>
 hipError_t launch_depth(bool perf, const WalkPlan &p, const WalkArgs &a, hipStream_t s) {
   if (p.split == 2) {
-    if constexpr (D <= 10) return launch_ds<D, 2>(perf, p, a, s);
+    if constexpr (D <= 10) return launch_ds<D, 2>(perf, p, a, s);  // D == 0: ragged
     return hipErrorInvalidValue;
   }
   return launch_ds<D, 1>(perf, p, a, s);
@@ -708,6 +839,7 @@ hipError_t launch_depth(bool perf, const WalkPlan &p, const WalkArgs &a, hipStre
 
 hipError_t launch_walk(bool perf, const Forest &f, const WalkPlan &p, const WalkArgs &a,
                        hipStream_t s) {
+  if (f.ragged) return launch_depth<0>(perf, p, a, s);
   switch (f.depth) {
     case 1: return launch_depth<1>(perf, p, a, s);
     case 2: return launch_depth<2>(perf, p, a, s);
@@ -752,6 +884,7 @@ hipError_t launch_leaves_depth(const WalkArgs &a, int G, int W, size_t lds, int 
 hipError_t launch_leaves(int depth, const WalkArgs &a, int G, int W, size_t lds, int row_tiles,
                          hipStream_t s) {
   switch (depth) {
+    case 0: return launch_leaves_depth<0>(a, G, W, lds, row_tiles, s);
     case 1: return launch_leaves_depth<1>(a, G, W, lds, row_tiles, s);
     case 2: return launch_leaves_depth<2>(a, G, W, lds, row_tiles, s);
     case 3: return launch_leaves_depth<3>(a, G, W, lds, row_tiles, s);
@@ -784,9 +917,9 @@ WalkArgs make_args(const Forest &f, const WalkPlan &p, const float *X, int64_t n
   a.n_pool = n;
   a.ld = ld;
   a.trees = static_cast<const char *>(f.d_trees);
-  a.ntrees = f.num_trees_padded;
+  a.ntrees = f.records;  // staged records: perfect trees or ragged slots
   a.chunk_trees = p.chunk_trees;
-  a.nchunks = (f.num_trees_padded + p.chunk_trees - 1) / p.chunk_trees;
+  a.nchunks = (f.records + p.chunk_trees - 1) / p.chunk_trees;
   a.F = f.num_features;
   a.vec4 = ((reinterpret_cast<uintptr_t>(X) & 15u) == 0 && (ld & 3) == 0) ? 1 : 0;
   a.nbuf = p.nbuf;
@@ -802,7 +935,8 @@ WalkArgs make_args(const Forest &f, const WalkPlan &p, const float *X, int64_t n
 // synchronously), G trees per lane.  Returns false if it does not fit.
 bool try_plan(const Forest &f, int64_t n_work, int cu_count, int S, int W, int mode, int G,
               int want_c, WalkPlan *p) {
-  if (!group_allowed(f.depth, G, S) || W < 1 || W > kMaxWaves) return false;
+  const int D = f.ragged ? 0 : f.depth;
+  if (!group_allowed(D, G, S) || W < 1 || W > kMaxWaves) return false;
   if (S == 2 && mode != 0) return false;  // groups are sized for register staging
   const size_t rb = f.rec_bytes;
   const int cpw = kLanes / S;
@@ -810,10 +944,10 @@ bool try_plan(const Forest &f, int64_t n_work, int cu_count, int S, int W, int m
   // tiles + the perf queue (C + NT entries, C = W * cpw, NT = 64 W)
   const size_t fixed = (size_t)W * (tile + (size_t)(cpw + kLanes) * sizeof(int32_t));
   const int nbuf = mode == 1 ? 2 : 1;
-  const int gs = G * S;
+  const int gs = f.ragged ? 1 : G * S;  // records per group (a ragged slot holds whole groups)
   if (fixed + (size_t)nbuf * gs * rb > kLdsBudget) return false;
   const size_t room = (kLdsBudget - fixed) / nbuf;
-  const int tpad = (f.num_trees_padded + gs - 1) / gs * gs;
+  const int tpad = (f.records + gs - 1) / gs * gs;
   int chunk_trees = (int)(room / rb) / gs * gs;
   WalkPlan q{};
   q.split = S;
@@ -872,7 +1006,9 @@ bool plan_walk(const Forest &f, int64_t n_work, int cu_count, WalkPlan *p, const
       for (int mode = 0; mode < 3; ++mode) {
         if (pass == 0 && want_b && want_b != (mode == 1 ? 2 : 1)) continue;
         for (int G : groups) {
-          if (pass == 0 && want_g && group_allowed(f.depth, want_g, S) && G != want_g) continue;
+          if (pass == 0 && want_g && group_allowed(f.ragged ? 0 : f.depth, want_g, S) &&
+              G != want_g)
+            continue;
           if (try_plan(f, n_work, cu_count, S, W, mode, G, pass == 0 ? want_c : 0, p)) return true;
         }
       }
@@ -911,12 +1047,14 @@ hipError_t launch_rows(const Forest &f, const float *X, int64_t n, int64_t ld, c
                        int32_t m, float *score_out, void *ws, int cu_count, hipStream_t s) {
   if (m <= 0) return hipSuccess;
   const size_t rb = f.rec_bytes;
+  const int D = f.ragged ? 0 : f.depth;
   const size_t tile = (size_t)f.num_features * Geo<1>::kRowBytes;
   int W = (int)std::min<int64_t>(4, (m + kLanes - 1) / kLanes);
   int G = 0;
   for (; W >= 1; --W) {
     for (int g : {16, 8, 4, 2, 1}) {
-      if (group_allowed(f.depth, g, 1) && W * tile + g * rb <= kLdsBudget) {
+      const size_t recs = f.ragged ? 1 : (size_t)g;  // records one group needs
+      if (group_allowed(D, g, 1) && W * tile + recs * rb <= kLdsBudget) {
         G = g;
         break;
       }
@@ -925,11 +1063,12 @@ hipError_t launch_rows(const Forest &f, const float *X, int64_t n, int64_t ld, c
   }
   if (!G) return hipErrorInvalidValue;  // excluded by the loader's limits
   const int row_tiles = (int)((m + (int64_t)W * kLanes - 1) / ((int64_t)W * kLanes));
-  const int tpad = f.num_trees_padded;  // a multiple of kTreePad, hence of G
-  int ct = (int)((kLdsBudget - W * tile) / rb) / G * G;
+  const int tpad = f.records;  // perfect: a multiple of kTreePad, hence of G
+  const int gr = f.ragged ? 1 : G;  // records per group
+  int ct = (int)((kLdsBudget - W * tile) / rb) / gr * gr;
   const int64_t want = 2 * (int64_t)cu_count;  // workgroups wanted in flight
   const int64_t chunks_wanted = (want + row_tiles - 1) / row_tiles;
-  const int cap = (int)std::max<int64_t>(G, (tpad / std::max<int64_t>(chunks_wanted, 1)) / G * G);
+  const int cap = (int)std::max<int64_t>(gr, (tpad / std::max<int64_t>(chunks_wanted, 1)) / gr * gr);
   ct = std::min(std::min(ct, cap), tpad);
   WalkArgs a{};
   a.X = X;
@@ -937,7 +1076,7 @@ hipError_t launch_rows(const Forest &f, const float *X, int64_t n, int64_t ld, c
   a.n_pool = n;
   a.ld = ld;
   a.trees = static_cast<const char *>(f.d_trees);
-  a.ntrees = tpad;
+  a.ntrees = tpad;  // records
   a.chunk_trees = ct;
   a.nchunks = (tpad + ct - 1) / ct;
   a.F = f.num_features;
@@ -947,8 +1086,9 @@ hipError_t launch_rows(const Forest &f, const float *X, int64_t n, int64_t ld, c
   a.rows_in = rows;
   a.score_out = score_out;
   a.leaves_out = static_cast<float *>(ws);
+  a.fold_trees = f.num_trees_padded;
   const size_t lds = W * tile + (size_t)ct * rb;
-  hipError_t e = launch_leaves(f.depth, a, G, W, lds, row_tiles, s);
+  hipError_t e = launch_leaves(D, a, G, W, lds, row_tiles, s);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(fold_kernel, dim3((unsigned)((m + 255) / 256)), dim3(256), 0, s, a);
   return hipGetLastError();

@@ -21,7 +21,8 @@ ML2_ERR_INVALID_ARG = 1
 ML2_ERR_UNSUPPORTED = 2
 ML2_ERR_OUT_OF_MEMORY = 3
 ML2_ERR_HIP = 4
-ML2_MAX_DEPTH = 12
+ML2_MAX_DEPTH = 32
+ML2_MAX_TREE_NODES = 2041
 ML2_MAX_FEATURES = 256
 ML2_MAX_TOPK = 16384
 
@@ -52,6 +53,7 @@ class ml2_ensemble_desc(ctypes.Structure):
         ("split_feature", ctypes.c_void_p),
         ("split_threshold", ctypes.c_void_p),
         ("leaf_value", ctypes.c_void_p),
+        ("default_left", ctypes.c_void_p),
     ]
 
 
@@ -172,10 +174,15 @@ def make_desc(ens):
         np.ascontiguousarray(ens.threshold, np.float32),
         np.ascontiguousarray(ens.value, np.float32),
     )
-    off, left, right, feat, thr, val = arrays
+    dl = getattr(ens, "default_left", None)
+    if dl is not None:
+        dl = np.ascontiguousarray(dl, np.uint8)
+        arrays = arrays + (dl,)
+    off, left, right, feat, thr, val = arrays[:6]
     d = ml2_ensemble_desc(int(off.shape[0] - 1), int(ens.num_features), float(ens.base_score),
                           off.ctypes.data, left.ctypes.data, right.ctypes.data,
-                          feat.ctypes.data, thr.ctypes.data, val.ctypes.data)
+                          feat.ctypes.data, thr.ctypes.data, val.ctypes.data,
+                          None if dl is None else dl.ctypes.data)
     return d, arrays
 
 

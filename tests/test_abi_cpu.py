@@ -32,7 +32,7 @@ def test_exports_every_declared_symbol():
 
 def test_header_constants_match_binding():
     text = open(HEADER).read()
-    for name in ("ML2_MAX_DEPTH", "ML2_MAX_FEATURES", "ML2_MAX_TOPK"):
+    for name in ("ML2_MAX_DEPTH", "ML2_MAX_TREE_NODES", "ML2_MAX_FEATURES", "ML2_MAX_TOPK"):
         m = re.search(rf"#define {name} (\d+)", text)
         assert m and int(m.group(1)) == getattr(ml2, name)
     for name, val in (("ML2_OK", 0), ("ML2_ERR_INVALID_ARG", 1), ("ML2_ERR_UNSUPPORTED", 2),
@@ -114,11 +114,28 @@ def test_load_rejects(case, status, needle):
     assert needle in msg
 
 
+def _caterpillar(depth):
+    """A tree whose right spine has `depth` splits (2 * depth + 1 nodes)."""
+    from tests.treeutil import ensemble_from_trees
+    tree = 1.0
+    for _ in range(depth):
+        tree = (0, 0.5, -1.0, tree)
+    return ensemble_from_trees([tree], num_features=4)
+
+
 def test_load_rejects_depth_beyond_limit():
-    depth = ml2.ML2_MAX_DEPTH + 1
-    e = gen.perfect_ensemble(1, 1, 1, depth, 4, 4, 0.5)
+    e = _caterpillar(ml2.ML2_MAX_DEPTH + 1)
     st, h, msg = _load_status(e)
     assert st == ml2.ML2_ERR_UNSUPPORTED and "depth" in msg and h is None
+
+
+def test_load_rejects_deep_tree_beyond_node_limit():
+    # deeper than the perfect layout and larger than a ragged chunk holds
+    e = gen.ragged_ensemble(1, 1, 1, 20, 4, 4, 0.5, p_split=1.0, decay=1.0,
+                            max_nodes=ml2.ML2_MAX_TREE_NODES + 2)
+    assert np.diff(e.offsets)[0] > ml2.ML2_MAX_TREE_NODES
+    st, h, msg = _load_status(e)
+    assert st == ml2.ML2_ERR_UNSUPPORTED and "nodes" in msg and h is None
 
 
 def test_load_null_arguments():

@@ -1,0 +1,132 @@
+"""GPU parity of the ragged layout (Table 3's deep models: 300 rounds up to
+depth 14, with XGBoost's per-node default directions for missing values)
+through the C ABI against the CPU oracle, bit for bit.  Inputs are seeded and
+synthetic; missing values are NaN in the hidden columns."""
+import json
+import os
+import sys
+
+import numpy as np
+import pytest
+
+import gen
+import oracle
+from tests.test_gpu_parity import check_pipeline
+from tests.test_gpu_rerank import check_rerank
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+from paper_2411_10764_amd import ml2  # noqa: E402
+from paper_2411_10764_amd.xgboost_json import load_xgboost_json  # noqa: E402
+
+DEV = "cuda:0"
+THREADS = gen.default_threads()
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _note(msg):
+    print(f"[gpu-ragged] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+def _paper_models(seed, F, K, trees=300, depth=14, max_nodes=400):
+    V = gen.perfect_ensemble(seed, 1, trees, 5, K, K, 0.5)
+    P = gen.ragged_ensemble(seed, 2, trees, depth, K, K, 0.1, max_nodes=max_nodes)
+    A = gen.ragged_ensemble(seed, 3, trees, depth, F, K, 0.1, max_nodes=max_nodes)
+    return V, P, A
+
+
+def test_depth_reported():
+    V, P, A = _paper_models(61, 32, 16, trees=40)
+    for e in (V, P, A):
+        h = ml2.ml2_load_ensemble(e)
+        want = max(int(max(_depth(e, t) for t in range(e.num_trees))), 1)
+        assert h.depth == want
+        h.free()
+
+
+def _depth(ens, t):
+    base = int(ens.offsets[t])
+    best, stack = 0, [(0, 0)]
+    while stack:
+        node, d = stack.pop()
+        l = int(ens.left[base + node])
+        if l < 0:
+            best = max(best, d)
+        else:
+            stack += [(l, d + 1), (int(ens.right[base + node]), d + 1)]
+    return best
+
+
+def test_paper_shaped_pipeline_with_missing_values():
+    n, F, K = 6000, 32, 16
+    V, _, A = _paper_models(62, F, K)
+    # P on all columns here so that the missing values reach a ragged model
+    P = gen.ragged_ensemble(62, 2, 300, 14, F, K, 0.1, max_nodes=400)
+    X = gen.features(62, n, F, K, missing=0.1)
+    _note(f"paper-shaped pipeline n={n} F={F}")
+    check_pipeline(V, P, X, 64)
+    rows = np.arange(0, n, 7, dtype=np.int32)
+    check_rerank(A, X, rows, 100)
+
+
+@pytest.mark.parametrize("split,waves,nbuf", [(1, 4, 1), (1, 8, 1), (2, 8, 1), (1, 4, 2),
+                                              (2, 4, 1), (1, 2, 1)])
+def test_ragged_plans(monkeypatch, split, waves, nbuf):
+    for key, val in (("SPLIT", split), ("WAVES", waves), ("NBUF", nbuf)):
+        monkeypatch.setenv(f"ML2_WALK_{key}", str(val))
+    n, F, K = 3000, 40, 20
+    V = gen.ragged_ensemble(63, 1, 60, 9, F, K, 0.5, base_score=0.2, max_nodes=300)
+    P = gen.ragged_ensemble(63, 2, 90, 14, F, K, 0.1, max_nodes=300)
+    X = gen.features(63, n, F, K, missing=0.2)
+    _note(f"ragged plan S={split} W={waves} nbuf={nbuf}")
+    check_pipeline(V, P, X, 50)
+
+
+def test_forced_ragged_layout_on_perfect_trees(monkeypatch):
+    """Perfect trees packed into ragged slots give the same results."""
+    monkeypatch.setenv("ML2_LAYOUT", "ragged")
+    w = gen.WORKLOADS["tiny"]
+    check_pipeline(w.validity(), w.perf(), w.features(), w.k)
+
+
+@pytest.mark.parametrize("max_nodes,depth", [(ml2.ML2_MAX_TREE_NODES, 32), (2041, 13),
+                                             (7, 3)])
+def test_ragged_tree_sizes(max_nodes, depth):
+    n, F, K = 2000, 24, 12
+    V = gen.ragged_ensemble(64, 1, 9, depth, F, K, 0.5, p_split=0.97, decay=0.99,
+                            max_nodes=max_nodes)
+    P = gen.ragged_ensemble(64, 2, 13, depth, F, K, 0.1, p_split=0.97, decay=0.99,
+                            max_nodes=max_nodes)
+    X = gen.features(64, n, F, K, missing=0.05)
+    _note(f"ragged sizes max_nodes={max_nodes} depth<={depth} "
+          f"largest tree {int(np.diff(P.offsets).max())} nodes")
+    check_pipeline(V, P, X, 40)
+
+
+def test_xgboost_fixture_on_gpu():
+    with open(os.path.join(GOLDEN, "xgboost_small.json")) as fh:
+        model = json.load(fh)
+    with open(os.path.join(GOLDEN, "xgboost_small_expected.json")) as fh:
+        exp = json.load(fh)
+    X = np.array([[np.nan if v == "nan" else v for v in row] for row in exp["inputs"]],
+                 np.float32)
+    e = ml2.ml2_load_ensemble(load_xgboost_json(model))
+    Xd = torch.from_numpy(X).to(DEV)
+    valid = torch.empty(X.shape[0], dtype=torch.uint8, device=DEV)
+    margin = torch.empty(X.shape[0], dtype=torch.float32, device=DEV)
+    ml2.ml2_score_validity(e, Xd, valid, margin)
+    torch.cuda.synchronize()
+    assert margin.cpu().numpy().tolist() == exp["margins"]
+    e.free()
+
+
+def test_explorer_with_ragged_models():
+    n, F, K, k, keep = 4000, 32, 16, 20, 10
+    V, P, A = _paper_models(65, F, K, trees=100)
+    X = gen.features(65, n, F, K, missing=0.1)
+    from tests.test_gpu_explorer import compare, run_rounds
+    pattern = [1, 0, 0, 1, 0, 0]
+    got = run_rounds(V, P, A, X, k, keep, pattern)
+    compare(got, oracle.explore(V, P, A, X, k, keep, len(pattern), THREADS))

@@ -66,8 +66,10 @@ def random_ragged_ensemble(rng, n_trees, max_depth, num_features, threshold_samp
 
 
 def leaf_paths(ens, t):
-    """[(conditions, value)] for tree t; a condition is (feature, thr, went_left)."""
+    """[(conditions, value)] for tree t; a condition is (feature, thr,
+    default_left, went_left)."""
     base = int(ens.offsets[t])
+    dl_arr = getattr(ens, "default_left", None)
     out = []
     stack = [(0, [])]
     while stack:
@@ -78,8 +80,9 @@ def leaf_paths(ens, t):
             out.append((conds, np.float32(ens.value[g])))
             continue
         f, th = int(ens.feature[g]), np.float32(ens.threshold[g])
-        stack.append((l, conds + [(f, th, True)]))
-        stack.append((r, conds + [(f, th, False)]))
+        dl = bool(dl_arr[g]) if dl_arr is not None else False
+        stack.append((l, conds + [(f, th, dl, True)]))
+        stack.append((r, conds + [(f, th, dl, False)]))
     return out
 
 
@@ -93,9 +96,12 @@ def path_predicate_leaves(ens, X):
         hits = np.zeros(n, np.int64)
         for conds, value in leaf_paths(ens, t):
             m = np.ones(n, bool)
-            for f, th, went_left in conds:
-                lt = X[:, f] < th
-                m &= lt if went_left else ~lt
+            for f, th, dl, went_left in conds:
+                # left: a present value below the threshold, or a missing
+                # value at a node whose default is left
+                x = X[:, f]
+                left = (x < th) | (np.isnan(x) & dl)
+                m &= left if went_left else ~left
             hits += m
             out[m, t] = value
         assert np.all(hits == 1), f"tree {t}: leaves do not partition the inputs"
