@@ -85,6 +85,25 @@ def copy_probe() -> None:
     print(json.dumps({"copy_probe_bytes": 4 * n, "launches": 5}))
 
 
+def mean_path(ens, X) -> float:
+    """Mean number of splits on a candidate's paths through all trees of a
+    ragged ensemble (its node visits), over the rows of X."""
+    dl = ens.default_left
+    total = 0.0
+    for t in range(ens.num_trees):
+        base = int(ens.offsets[t])
+        node = np.zeros(X.shape[0], np.int64)
+        active = ens.left[base + node] >= 0
+        while active.any():
+            g = base + node[active]
+            x = X[np.flatnonzero(active), ens.feature[g]]
+            left = (x < ens.threshold[g]) | (np.isnan(x) & (dl[g] != 0))
+            node[active] = np.where(left, ens.left[g], ens.right[g])
+            total += float(active.sum())
+            active = ens.left[base + node] >= 0
+    return total / X.shape[0]
+
+
 def cpu_baseline(w, rows: int):
     import gen
     import oracle
@@ -185,7 +204,7 @@ def main() -> int:
     host = np.empty((chunk, w.F), np.float32)
     for r0 in range(0, w.n, chunk):
         m = min(chunk, w.n - r0)
-        gen.features(w.seed, m, w.F, w.K, row0=r0, out=host[:m])
+        gen.features(w.seed, m, w.F, w.K, row0=r0, out=host[:m], missing=w.missing)
         X[r0:r0 + m].copy_(torch.from_numpy(host[:m]))
     torch.cuda.synchronize()
     del host
@@ -260,6 +279,12 @@ def main() -> int:
         alg_bytes += 4.0 * w.F * w.k + 8.0 * w.keep
     visits_v = w.n * w.v_trees * w.v_depth
     visits_p = n_valid * w.p_trees * w.p_depth
+    if w.ragged:  # node visits are the paths' lengths, measured on accepted rows
+        sample = np.flatnonzero(valid)[:4096].astype(np.int64)
+        per_row = mean_path(w.perf(), w.features(rows=sample))
+        visits_p = int(round(n_valid * per_row))
+        _log(f"ragged P: {per_row / w.p_trees:.2f} splits per tree on average "
+             f"(depth <= {w.p_depth})")
     sha = _kernel_sha()
     perf_visits_per_s = visits_p / (t_perf / 1000.0)
     traffic = _traffic(sha) if w.name == "roofline" else None
@@ -276,7 +301,7 @@ def main() -> int:
         "traffic": traffic,
         "traffic_unit": "bytes per launch (HBM read + write, copy-calibrated rocprofv3 counters)",
         "work_per_launch": f"{visits_p} node visits ({n_valid} accepted x {w.p_trees} trees "
-                           f"x depth {w.p_depth})",
+                           + (f"x measured mean path)" if w.ragged else f"x depth {w.p_depth})"),
         "launch_ms": t_perf,
         "validity_kernel": {"achieved": visits_v / (t_val / 1000.0) / 1e12, "launch_ms": t_val,
                             "frac": visits_v / (t_val / 1000.0) / VISIT_PEAK_PER_S},
@@ -292,7 +317,9 @@ def main() -> int:
         "data": "synthetic (seeded knob + lognormal features, random perfect trees)",
         "config": {"workload": w.name, "candidates": w.n, "features": w.F,
                    "knob_features": w.K, "validity": f"{w.v_trees} trees x depth {w.v_depth}",
-                   "perf": f"{w.p_trees} trees x depth {w.p_depth}", "k": w.k,
+                   "perf": f"{w.p_trees} trees x depth {'<= ' if w.ragged else ''}{w.p_depth}"
+                           + (" (ragged, default directions)" if w.ragged else ""),
+                   "k": w.k, "missing_hidden_fraction": w.missing,
                    "seed": w.seed, "invalid_fraction": 1 - n_valid / w.n},
         **({"second_level": {"model_a": f"{w.a_trees} trees x depth {w.a_depth} over {w.F} "
                                         f"features", "keep": w.keep,

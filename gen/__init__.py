@@ -209,6 +209,12 @@ class Workload:
     a_depth: int = 0
     keep: int = 0
     visible_only: bool = False
+    # Paper-shaped models (Table 3): P and A as ragged trees of at most
+    # p_depth / a_depth levels with default directions, grown with
+    # ragged_ensemble's defaults; hidden values missing with this probability.
+    ragged: bool = False
+    ragged_max_nodes: int = 255
+    missing: float = 0.0
 
     def _vp_features(self) -> int:
         return self.K if self.visible_only else self.F
@@ -218,15 +224,23 @@ class Workload:
                                 self._vp_features(), self.K, 0.5, self.base_v)
 
     def perf(self) -> Ensemble:
+        if self.ragged:
+            return ragged_ensemble(self.seed, STREAM_PERF, self.p_trees, self.p_depth,
+                                   self._vp_features(), self.K, 0.1,
+                                   max_nodes=self.ragged_max_nodes)
         return perfect_ensemble(self.seed, STREAM_PERF, self.p_trees, self.p_depth,
                                 self._vp_features(), self.K, 0.1, 0.0)
 
     def second_level(self) -> Ensemble:
         assert self.a_trees > 0, f"workload {self.name} has no second-level model"
+        if self.ragged:
+            return ragged_ensemble(self.seed, STREAM_SECOND_LEVEL, self.a_trees, self.a_depth,
+                                   self.F, self.K, 0.1, max_nodes=self.ragged_max_nodes)
         return perfect_ensemble(self.seed, STREAM_SECOND_LEVEL, self.a_trees, self.a_depth,
                                 self.F, self.K, 0.1, 0.0)
 
     def features(self, rows=None, **kw) -> np.ndarray:
+        kw.setdefault("missing", self.missing)
         return features(self.seed, self.n, self.F, self.K, rows=rows, **kw)
 
 
@@ -251,5 +265,13 @@ WORKLOADS = {
     # hidden columns; k = (alpha+1)N = 1024 held, N = 512 kept (alpha = 1).
     "explorer": Workload("explorer", 16777216, 128, 64, 300, 6, 1000, 8, 1024, 6,
                          a_trees=300, a_depth=12, keep=512, visible_only=True),
+    # The models as Table 3 sizes them: V 300 rounds of depth 5; P and A 300
+    # rounds of depth up to 14 (ragged, default directions for missing
+    # values; trees of about 100 nodes, as trained on a few hundred profiled
+    # configurations); 5 % of the hidden values missing; (alpha+1)N = 20
+    # held and N = 10 kept (Section 3).
+    "paper": Workload("paper", 16777216, 128, 64, 300, 5, 300, 14, 20, 7,
+                      a_trees=300, a_depth=14, keep=10, visible_only=True, ragged=True,
+                      missing=0.05),
 }
 CALIBRATION_ROWS = 65536

@@ -339,6 +339,13 @@ struct RWalks {
     for (int g = 0; g < H; ++g)
       leaf[g] = *reinterpret_cast<const float *>(slot + vbias + (u[g] >> 1));
   }
+  // Every walk of this lane is on a leaf (whose first word is kLeafWord).
+  __device__ __forceinline__ bool at_leaves() const {
+    bool all = true;
+#pragma unroll
+    for (int g = 0; g < H; ++g) all = all && nd[g].x == kLeafWord;
+    return all;
+  }
   __device__ __forceinline__ float fold(float m) const {
 #pragma unroll
     for (int g = 0; g < H; ++g) m = m + leaf[g];
@@ -349,6 +356,7 @@ struct RWalks {
     for (int g = 0; g < H; ++g) m = m + from_upper_half(leaf[g]);
     return m;
   }
+  static constexpr uint32_t kLeafWord = (uint32_t)(-8) << 9;  // offset -8, feature 0
 };
 
 // Ragged chunk slot header (see ml2_internal.h), read from LDS into scalars.
@@ -367,7 +375,9 @@ __device__ __forceinline__ SlotHead slot_head(const char *slot) {
 }
 
 // One group of a ragged slot: the G trees whose root offsets start at
-// `roots` (in LDS), walked `depth` steps (the slot's deepest path).
+// `roots` (in LDS), walked until every lane of the wave is on leaves, at
+// most `depth` steps (the slot's deepest path).  Leaves step onto
+// themselves, so stopping at any point past that gives the same leaves.
 template <int G, int S, typename Done>
 __device__ __forceinline__ void walk_group_ragged(const char *slot, const uint32_t *roots,
                                                   int depth, uint32_t vbias,
@@ -377,6 +387,7 @@ __device__ __forceinline__ void walk_group_ragged(const char *slot, const uint32
     A.u[0] = roots[0];
     A.read_nodes(slot);
     for (int l = 0; l < depth; ++l) {
+      if (__all(A.at_leaves())) break;
       A.read_features(tile_lane);
       A.descend();
       A.read_nodes(slot);
@@ -395,6 +406,7 @@ __device__ __forceinline__ void walk_group_ragged(const char *slot, const uint32
     B.read_nodes(slot);
     __builtin_amdgcn_sched_barrier(0);
     for (int l = 0; l < depth; ++l) {
+      if (__all(A.at_leaves() && B.at_leaves())) break;
       A.read_features(tile_lane);
       __builtin_amdgcn_sched_barrier(0);
       B.read_features(tile_lane);
