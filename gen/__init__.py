@@ -273,5 +273,10 @@ WORKLOADS = {
     "paper": Workload("paper", 16777216, 128, 64, 300, 5, 300, 14, 20, 7,
                       a_trees=300, a_depth=14, keep=10, visible_only=True, ragged=True,
                       missing=0.05),
+    # Diagnostic, not a benchmark configuration: the 16M x 128 pool with
+    # small ensembles (V and P 40 trees of depth 5, about 300 node visits
+    # per candidate), where reading the pool from HBM, not walking trees,
+    # bounds the step.
+    "hbm": Workload("hbm", 16777216, 128, 64, 40, 5, 40, 5, 1024, 8),
 }
 CALIBRATION_ROWS = 65536

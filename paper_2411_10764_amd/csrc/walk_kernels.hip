@@ -33,6 +33,7 @@
 #include <stdlib.h>
 
 #include <algorithm>
+#include <type_traits>
 
 #include "ml2_internal.h"
 
@@ -117,10 +118,6 @@ __device__ __forceinline__ void load_row(const WalkArgs &a, int64_t row, char *d
 constexpr int kRowVecs = 32;
 constexpr int kRowBatch = 8;
 
-struct RowHead {
-  f32x4 v[kRowBatch];
-};
-
 __device__ __forceinline__ const f32x4 *row_src(const WalkArgs &a, int64_t row) {
   const int64_t rr = (row >= 0 && row < a.n_pool) ? row : 0;
   return reinterpret_cast<const f32x4 *>(a.X + rr * a.ld);
@@ -149,20 +146,6 @@ __device__ __forceinline__ void row_batch_store(const WalkArgs &a, int b,
       *reinterpret_cast<float *>(dst + (4 * q + 2) * RW) = v[k].z;
       *reinterpret_cast<float *>(dst + (4 * q + 3) * RW) = v[k].w;
     }
-  }
-}
-
-// Write batch h of the row (already in `head`) and the lane half's further
-// batches h+S, h+2S, ... into the tile.
-template <int S>
-__device__ __forceinline__ void row_commit(const WalkArgs &a, int64_t row, const RowHead &head,
-                                           int h, char *dst) {
-  row_batch_store<S>(a, h, head.v, dst);
-  const int nb = (a.F / 4 + kRowBatch - 1) / kRowBatch;
-  for (int b = h + S; b < nb; b += S) {
-    f32x4 v[kRowBatch];
-    row_batch_load(a, row, b, v);
-    row_batch_store<S>(a, b, v, dst);
   }
 }
 
@@ -512,6 +495,39 @@ struct Stage {
   u32x4 r[K][R];  // registers: the next K chunks
 };
 
+// Row prefetch: batches h, h+S, ..., h+E*S of a row (the lane half's first
+// E+1 batches) in registers.  With the whole ensemble in one chunk nothing is
+// restaged, the staging registers are dead, and E extra batches take their
+// place, so that the next round's rows are (for F <= 128 with S = 2: fully)
+// in flight while the current round is walked.
+template <int S, int K, int R>
+constexpr int row_extra_batches() {
+  return S == 2 ? (K * R) / kRowBatch : 0;  // one lane per candidate: no room
+}
+
+template <int S, int E>
+struct RowPrefetch {
+  f32x4 v[E + 1][kRowBatch];
+
+  __device__ __forceinline__ void load(const WalkArgs &a, int64_t row, int h) {
+#pragma unroll
+    for (int e = 0; e <= E; ++e) row_batch_load(a, row, h + e * S, v[e]);
+  }
+  // Write the prefetched batches into the tile, then load and write the lane
+  // half's remaining batches.
+  __device__ __forceinline__ void commit(const WalkArgs &a, int64_t row, int h,
+                                         char *dst) const {
+#pragma unroll
+    for (int e = 0; e <= E; ++e) row_batch_store<S>(a, h + e * S, v[e], dst);
+    const int nb = (a.F / 4 + kRowBatch - 1) / kRowBatch;
+    for (int b = h + (E + 1) * S; b < nb; b += S) {
+      f32x4 w[kRowBatch];
+      row_batch_load(a, row, b, w);
+      row_batch_store<S>(a, b, w, dst);
+    }
+  }
+};
+
 // Length of the cyclic chunk sequence: with register staging it is padded
 // with empty chunks to a multiple of K, so that set j always holds a chunk
 // whose index is j+1 modulo K and every set index is a compile-time constant.
@@ -603,6 +619,31 @@ __device__ __forceinline__ float walk_all(const WalkArgs &a, Stage<K, R> &s,
   return m;
 }
 
+// The round loop of a walk kernel, by regime.  kAny decides row prefetch and
+// staging at run time.  With S = 2 the kernels run a separate loop for
+// prefetched rows with a streamed ensemble and one with a resident ensemble
+// (one chunk), so that no loop merges register values from another: where a
+// loop did, the compiler copied the prefetched rows at the merge and, to do
+// so, waited for every load in flight before each walk.  With S = 1 the
+// kernels are near their register limit and keep the single loop.
+constexpr int kAny = 0;
+constexpr int kStreamed = 1;
+constexpr int kResident = 2;
+
+template <int S, typename Rounds>
+__device__ __forceinline__ void dispatch_rounds(const WalkArgs &a, Rounds &rounds) {
+  if constexpr (S == 2) {
+    if (!a.rowpf)
+      rounds(std::integral_constant<int, kAny>{});
+    else if (a.nchunks == 1)
+      rounds(std::integral_constant<int, kResident>{});
+    else
+      rounds(std::integral_constant<int, kStreamed>{});
+  } else {
+    rounds(std::integral_constant<int, kAny>{});
+  }
+}
+
 // With S = 2 a kernel must leave room for two waves per SIMD (256 VGPRs).
 template <int D, int G, int S>
 __global__ void __launch_bounds__(kLanes *kMaxWaves) __attribute__((amdgpu_waves_per_eu(S, S)))
@@ -623,24 +664,32 @@ validity_kernel(WalkArgs a) {
   char *tile_lane = smem + wave * tile_bytes + 4 * cl;
   const int64_t ntiles = (a.n + CPW - 1) / CPW;
   stage_prime(a, RB, st);
-  RowHead head;
-  if (a.rowpf) row_batch_load(a, ((int64_t)blockIdx.x * W + wave) * CPW + cl, h, head.v);
-  for (int64_t tg = blockIdx.x; tg * W < ntiles; tg += gridDim.x) {
-    const int64_t row = (tg * W + wave) * CPW + cl;
-    const bool active = row < a.n;
-    if (a.rowpf) {
-      row_commit<S>(a, row, head, h, tile_lane);
-      row_batch_load(a, ((tg + gridDim.x) * W + wave) * CPW + cl, h, head.v);
-    } else if (active && h == 0) {
-      load_row<S>(a, row, tile_lane);
+  auto rounds = [&](auto mode) {
+    constexpr int M = decltype(mode)::value;
+    constexpr int E = M == kResident ? row_extra_batches<S, kValiditySets, Geo<S>::kStageRegs>()
+                                     : 0;
+    RowPrefetch<S, E> pf;
+    const bool pfr = M != kAny || a.rowpf;  // rows prefetched
+    if (pfr) pf.load(a, ((int64_t)blockIdx.x * W + wave) * CPW + cl, h);
+    for (int64_t tg = blockIdx.x; tg * W < ntiles; tg += gridDim.x) {
+      const int64_t row = (tg * W + wave) * CPW + cl;
+      const bool active = row < a.n;
+      if (pfr) {
+        pf.commit(a, row, h, tile_lane);
+        pf.load(a, ((tg + gridDim.x) * W + wave) * CPW + cl, h);
+      } else if (active && h == 0) {
+        load_row<S>(a, row, tile_lane);
+      }
+      __syncthreads();
+      const float m = M == kResident ? walk_chunk<D, G, S>(st.cur, a.ntrees, tile_lane, h, a.base)
+                                     : walk_all<D, G, S>(a, st, tile_lane, h);
+      if (active && h == 0) {
+        __builtin_nontemporal_store((uint8_t)((m > 0.0f) ? 1 : 0), a.valid_out + row);
+        if (a.margin_out) __builtin_nontemporal_store(m, a.margin_out + row);
+      }
     }
-    __syncthreads();
-    const float m = walk_all<D, G, S>(a, st, tile_lane, h);
-    if (active && h == 0) {
-      __builtin_nontemporal_store((uint8_t)((m > 0.0f) ? 1 : 0), a.valid_out + row);
-      if (a.margin_out) __builtin_nontemporal_store(m, a.margin_out + row);
-    }
-  }
+  };
+  dispatch_rounds<S>(a, rounds);
 }
 
 template <int D, int G, int S>
@@ -703,21 +752,28 @@ perf_kernel(WalkArgs a) {
     __syncthreads();
     return r;
   };
-  RowHead head;
-  int32_t row = next_rows();
-  if (a.rowpf) row_batch_load(a, row, h, head.v);
-  for (;;) {
-    if (__syncthreads_or(row >= 0) == 0) break;
-    if (a.rowpf)
-      row_commit<S>(a, row, head, h, tile_lane);
-    else if (row >= 0 && h == 0)
-      load_row<S>(a, row, tile_lane);
-    const int32_t nrow = next_rows();  // ends with a barrier: the tiles are complete
-    if (a.rowpf) row_batch_load(a, nrow, h, head.v);
-    const float m = walk_all<D, G, S>(a, st, tile_lane, h);
-    if (row >= 0 && h == 0) __builtin_nontemporal_store(m, a.score_out + row);
-    row = nrow;
-  }
+  auto rounds = [&](auto mode) {  // see validity_kernel
+    constexpr int M = decltype(mode)::value;
+    constexpr int E = M == kResident ? row_extra_batches<S, kPerfSets, Geo<S>::kStageRegs>() : 0;
+    RowPrefetch<S, E> pf;
+    const bool pfr = M != kAny || a.rowpf;  // rows prefetched
+    int32_t row = next_rows();
+    if (pfr) pf.load(a, row, h);
+    for (;;) {
+      if (__syncthreads_or(row >= 0) == 0) break;
+      if (pfr)
+        pf.commit(a, row, h, tile_lane);
+      else if (row >= 0 && h == 0)
+        load_row<S>(a, row, tile_lane);
+      const int32_t nrow = next_rows();  // ends with a barrier: the tiles are complete
+      if (pfr) pf.load(a, nrow, h);
+      const float m = M == kResident ? walk_chunk<D, G, S>(st.cur, a.ntrees, tile_lane, h, a.base)
+                                     : walk_all<D, G, S>(a, st, tile_lane, h);
+      if (row >= 0 && h == 0) __builtin_nontemporal_store(m, a.score_out + row);
+      row = nrow;
+    }
+  };
+  dispatch_rounds<S>(a, rounds);
 }
 
 // Tree-parallel walk of a short row list (the second level): workgroup
@@ -802,8 +858,7 @@ constexpr bool group_allowed(int d, int g, int s) {
          : d == 9 ? (g == 1 || g == 2)
          : d == 10 ? (g == 1)
                    : false;
-  return d <= 7 ? (g == 8 || g == 16)
-       : d <= 9 ? (g == 4 || g == 8)
+  return d <= 9 ? (g == 4 || g == 8)
        : d == 10 ? (g == 2 || g == 4)
                  : (g == 1 || g == 2);
 }
