@@ -165,6 +165,47 @@ def explore(args, w, X, v, p, dev) -> int:
     return 0
 
 
+def _print(out) -> int:
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+def out_hbm(w, args, value, ms_per_step, t_val, t_perf, t_topk, n_valid, alg_bytes):
+    """The HBM-bound diagnostic: small ensembles, so reading the pool bounds
+    the step.  The roofline object covers the validity launch, which reads
+    every row once (4F bytes) and writes the mask (1 byte)."""
+    val_bytes = (4.0 * w.F + 1.0) * w.n
+    perf_bytes = 4.0 * w.F * n_valid + 1.0 * w.n + 4.0 * w.n  # accepted rows, mask, scores
+    achieved = val_bytes / (t_val / 1000.0) / 1e9
+    return {
+        "metric": METRIC, "value": value, "unit": "candidates/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded knob + lognormal features, random perfect trees)",
+        "config": {"workload": w.name, "diagnostic": "HBM-bound: not a benchmark configuration",
+                   "candidates": w.n, "features": w.F,
+                   "validity": f"{w.v_trees} trees x depth {w.v_depth}",
+                   "perf": f"{w.p_trees} trees x depth {w.p_depth}", "k": w.k, "seed": w.seed,
+                   "invalid_fraction": 1 - n_valid / w.n},
+        "roofline": {
+            "bound": "hbm", "kernel": "validity_kernel (reads the pool once)",
+            "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+            "work_per_launch": f"{val_bytes:.4g} bytes ({w.n} rows x {4 * w.F} B + mask)",
+            "launch_ms": t_val,
+            "perf_kernel": {"achieved": perf_bytes / (t_perf / 1000.0) / 1e9,
+                            "launch_ms": t_perf,
+                            "bytes": perf_bytes},
+            "step": {"algorithmic_bytes": alg_bytes,
+                     "achieved_gbs": alg_bytes / (ms_per_step / 1000.0) / 1e9,
+                     "frac": alg_bytes / (ms_per_step / 1000.0) / 1e9 / HBM_PEAK_GBS},
+        },
+        "hbm_frac": alg_bytes / (ms_per_step / 1000.0) / 1e9 / HBM_PEAK_GBS,
+        "kernel_ms": {"validity": t_val, "perf": t_perf, "topk": t_topk},
+        "cpu_baseline": None,
+    }
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -288,6 +329,9 @@ def main() -> int:
     sha = _kernel_sha()
     perf_visits_per_s = visits_p / (t_perf / 1000.0)
     traffic = _traffic(sha) if w.name == "roofline" else None
+    if w.name == "hbm":
+        return _print(out_hbm(w, args, value, ms_per_step, t_val, t_perf, t_topk, n_valid,
+                              alg_bytes))
     roofline = {
         "bound": "alu",
         "kernel": "perf_kernel (model P walk over accepted candidates)",
