@@ -201,7 +201,7 @@ def test_depth_and_width_limits(depth, F, trees):
 
 
 @pytest.mark.parametrize("split,group,waves,nbuf,chunk,depth", [
-    (1, 16, 4, 1, 0, 7), (1, 8, 8, 1, 0, 7), (1, 8, 4, 2, 0, 7), (1, 8, 4, 1, 16, 7),
+    (1, 4, 4, 1, 0, 7), (1, 8, 8, 1, 0, 7), (1, 8, 4, 2, 0, 7), (1, 8, 4, 1, 16, 7),
     (2, 8, 8, 1, 0, 7), (2, 4, 8, 1, 16, 7), (2, 4, 4, 1, 0, 7), (2, 8, 8, 1, 32, 7),
     (2, 4, 8, 1, 16, 6), (2, 2, 8, 1, 0, 8), (2, 1, 8, 1, 0, 9), (2, 1, 8, 1, 0, 10),
 ])
@@ -217,6 +217,21 @@ def test_walk_plans(monkeypatch, split, group, waves, nbuf, chunk, depth):
     X = gen.features(31, 3001, F, K)
     _note(f"plan S={split} G={group} W={waves} nbuf={nbuf} chunk={chunk} depth={depth}")
     check_pipeline(V, P, X, 64)
+
+
+@pytest.mark.parametrize("F,ld,trees", [(40, 40, 30), (128, 128, 48), (128, 131, 20),
+                                         (132, 132, 16), (6, 6, 1)])
+def test_resident_ensemble(monkeypatch, F, ld, trees):
+    """Ensembles that fit one chunk (never restaged) with two lanes per
+    candidate: rows prefetched whole into the staging registers where they
+    are aligned and at most 128 wide, loaded directly otherwise."""
+    monkeypatch.setenv("ML2_WALK_SPLIT", "2")
+    K = max(F // 2, 1)
+    V = gen.perfect_ensemble(33, 1, trees, 5, F, K, 0.5)
+    P = gen.perfect_ensemble(33, 2, trees, 4, F, K, 0.1)
+    X = gen.features(33, 5003, F, K)
+    _note(f"resident F={F} ld={ld} trees={trees}")
+    check_pipeline(V, P, X, 40, ld=ld)
 
 
 def test_perf_without_mask():
