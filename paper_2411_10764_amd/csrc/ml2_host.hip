@@ -187,7 +187,7 @@ void pack_ragged(const std::vector<TreeView> &views, const std::vector<int> &dep
                  RaggedPack *out) {
   constexpr uint32_t CAP = ml2::kRaggedChunkBytes;
   constexpr int GRP = ml2::kRaggedGroup;
-  const uint32_t leaf_word0 = (uint32_t)(-8) << 9;  // offset -8: the node itself
+  const uint32_t leaf_word0 = 0x7FFFFFu << 8;  // offset -1: the node itself
   const uint32_t nan_bits = 0x7FC00000u;
   size_t t = 0;
   int32_t tree_index = 0;
@@ -219,7 +219,7 @@ void pack_ragged(const std::vector<TreeView> &views, const std::vector<int> &dep
     uint32_t next = 0;  // next free node index in the slot
     std::vector<int32_t> order;
     for (size_t i = 0; i < ntr; ++i) {
-      root[i] = head + 8u * next;
+      root[i] = head / 8u + next;
       if (i >= real) {  // padding: one leaf of value -0.0
         node[next] = make_uint2(leaf_word0, nan_bits);
         val[next] = -0.0f;
@@ -247,17 +247,19 @@ void pack_ragged(const std::vector<TreeView> &views, const std::vector<int> &dep
           node[j] = make_uint2(leaf_word0, nan_bits);
           val[j] = tv.val[o];
         } else {
-          const int32_t rel = 8 * (newid[(size_t)tv.left[o]] - (int32_t)k);
+          const int32_t rel = newid[(size_t)tv.left[o]] - (int32_t)k;  // nodes, > 0
           const uint32_t dl = (tv.dl && tv.dl[o]) ? 1u : 0u;
           uint32_t tb;
           memcpy(&tb, &tv.thr[o], 4);
-          node[j] = make_uint2(((uint32_t)rel << 9) | (dl << 8) | (uint32_t)tv.feat[o], tb);
+          node[j] = make_uint2((dl << 31) | (((uint32_t)rel & 0x7FFFFFu) << 8) |
+                                   (uint32_t)tv.feat[o],
+                               tb);
           val[j] = 0.0f;
         }
       }
       next += (uint32_t)order.size();
     }
-    // values are addressed as vbias + (node byte offset) / 2
+    // the value of the node with index u (8-byte units) is at byte vbias + 4u
     const uint32_t hdr[4] = {(uint32_t)ntr, (uint32_t)depth, vals - head / 2, (uint32_t)tree_index};
     memcpy(slot, hdr, sizeof hdr);
     tree_index += (int32_t)ntr;

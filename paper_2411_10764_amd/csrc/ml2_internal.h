@@ -31,13 +31,14 @@ constexpr int kMaxPerfectDepth = 12;  // deeper ensembles use the ragged layout
 // fixed slot of kRaggedChunkBytes bytes:
 //   byte 0   uint4 {trees in the chunk (a multiple of kRaggedGroup), deepest
 //            path of those trees, vbias, global index of the chunk's first
-//            tree}; the value of the node at byte offset u is at vbias + u/2
-//   byte 16  uint32 root byte offset of each tree (from the slot start)
+//            tree}; the value of the node with index u is at byte vbias + 4u
+//   byte 16  uint32 root node index of each tree (node u at byte 8u of the
+//            slot)
 //   then 8-byte nodes, each tree breadth-first (siblings adjacent):
-//     word 0: bits 31..9 signed byte offset from the node to its left child
-//             (the right child follows it), bit 8 default-left, bits 7..0
-//             split feature; word 1: threshold bits
-//     a leaf steps back onto itself: offset -8, threshold NaN, so x < t is
+//     word 0: bit 31 default-left, bits 30..8 signed offset in nodes from
+//             the node to its left child (the right child follows it),
+//             bits 7..0 split feature; word 1: threshold bits
+//     a leaf steps back onto itself: offset -1, threshold NaN, so x < t is
 //     false, it "goes right" to itself and a lockstep walk may run past it
 //   then one float per node (the leaf values; 0 for splits)
 // Trees padded onto a chunk are single leaves of value -0.0.

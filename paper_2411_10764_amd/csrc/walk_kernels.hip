@@ -289,10 +289,11 @@ struct Walks {
   }
 };
 
-// H walks of one half over a ragged chunk slot: u is the byte offset of the
-// current node in the slot.  One step: x < t goes left, a missing x goes
-// left where the node's default is left, else right; the right child follows
-// the left one, and a leaf steps onto itself.
+// H walks of one half over a ragged chunk slot: u is the index of the
+// current 8-byte node in the slot.  One step: x < t goes left, a missing x
+// goes left where the node's default is left, else right; the right child
+// follows the left one (u <- u + offset + [right]), and a leaf steps onto
+// itself.
 template <int H, int S>
 struct RWalks {
   uint32_t u[H];
@@ -302,25 +303,30 @@ struct RWalks {
 
   __device__ __forceinline__ void read_nodes(const char *slot) {
 #pragma unroll
-    for (int g = 0; g < H; ++g) nd[g] = *reinterpret_cast<const uint2 *>(slot + u[g]);
+    for (int g = 0; g < H; ++g) nd[g] = *reinterpret_cast<const uint2 *>(slot + 8u * u[g]);
   }
   __device__ __forceinline__ void read_features(const char *tile_lane) {
 #pragma unroll
-    for (int g = 0; g < H; ++g)
-      x[g] = *reinterpret_cast<const float *>(tile_lane + ((nd[g].x & 0xFFu) << Geo<S>::kRowShift));
+    for (int g = 0; g < H; ++g) {
+      uint32_t f;
+      asm("v_bfe_u32 %0, %1, 0, 8" : "=v"(f) : "v"(nd[g].x));
+      x[g] = *reinterpret_cast<const float *>(tile_lane + (f << Geo<S>::kRowShift));
+    }
   }
   __device__ __forceinline__ void descend() {
 #pragma unroll
     for (int g = 0; g < H; ++g) {
       const float t = __uint_as_float(nd[g].y);
-      const bool left = (x[g] < t) || ((nd[g].x & 0x100u) != 0u && __builtin_isnan(x[g]));
-      u[g] = u[g] + (uint32_t)((int32_t)nd[g].x >> 9) + (left ? 0u : 8u);
+      const bool missing_left = (int32_t)nd[g].x < 0 && __builtin_isnan(x[g]);
+      const bool right = !(x[g] < t) && !missing_left;
+      const int32_t off = (int32_t)(nd[g].x << 1) >> 9;  // bits 30..8, signed
+      u[g] = u[g] + (uint32_t)off + (right ? 1u : 0u);
     }
   }
   __device__ __forceinline__ void read_leaves(const char *slot, uint32_t vbias) {
 #pragma unroll
     for (int g = 0; g < H; ++g)
-      leaf[g] = *reinterpret_cast<const float *>(slot + vbias + (u[g] >> 1));
+      leaf[g] = *reinterpret_cast<const float *>(slot + vbias + 4u * u[g]);
   }
   // Every walk of this lane is on a leaf (whose first word is kLeafWord).
   __device__ __forceinline__ bool at_leaves() const {
@@ -339,7 +345,7 @@ struct RWalks {
     for (int g = 0; g < H; ++g) m = m + from_upper_half(leaf[g]);
     return m;
   }
-  static constexpr uint32_t kLeafWord = (uint32_t)(-8) << 9;  // offset -8, feature 0
+  static constexpr uint32_t kLeafWord = 0x7FFFFFu << 8;  // offset -1, feature 0
 };
 
 // Ragged chunk slot header (see ml2_internal.h), read from LDS into scalars.
@@ -370,8 +376,8 @@ __device__ __forceinline__ void walk_group_ragged(const char *slot, const uint32
     A.u[0] = roots[0];
     A.read_nodes(slot);
     for (int l = 0; l < depth; ++l) {
-      if (__all(A.at_leaves())) break;
       A.read_features(tile_lane);
+      if (__all(A.at_leaves())) break;
       A.descend();
       A.read_nodes(slot);
     }
@@ -389,11 +395,13 @@ __device__ __forceinline__ void walk_group_ragged(const char *slot, const uint32
     B.read_nodes(slot);
     __builtin_amdgcn_sched_barrier(0);
     for (int l = 0; l < depth; ++l) {
-      if (__all(A.at_leaves() && B.at_leaves())) break;
+      // the exit test follows the feature reads, so that it does not hold
+      // them back until every node read has landed
       A.read_features(tile_lane);
       __builtin_amdgcn_sched_barrier(0);
       B.read_features(tile_lane);
       __builtin_amdgcn_sched_barrier(0);
+      if (__all(A.at_leaves() && B.at_leaves())) break;
       A.descend();
       A.read_nodes(slot);
       __builtin_amdgcn_sched_barrier(0);
