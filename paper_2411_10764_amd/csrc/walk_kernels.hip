@@ -18,7 +18,12 @@
 //     breadth-ordered nodes of that level.
 //   * The ensemble streams through one LDS buffer in chunks of whole trees.
 //     The next chunks are fetched into registers while the current one is
-//     walked, then written to LDS between two barriers.
+//     walked, then written to LDS between two barriers.  An ensemble that
+//     fits one chunk stays resident, and with S = 2 the staging registers
+//     then carry the next round's rows instead.
+//   * Rows are fetched for the next round while the current one is walked
+//     (aligned rows of at most 128 features), one candidate per lane, so
+//     that each lane writes its own column of the transposed tile.
 //   * Each lane walks G trees at once, as two halves offset by half a level:
 //     while one half waits for its node (or feature) reads, the other half
 //     issues its own.  Leaves are added to the running margin in tree-index
