@@ -464,10 +464,50 @@ __device__ __forceinline__ void walk_group(const char *rec, const char *tile_lan
   }
 }
 
+// Calls of walk_chunk's `after` for a chunk of ntr records: one per group
+// of perfect trees, one per ragged slot.
+template <int D, int G, int S>
+__device__ __forceinline__ int walk_groups(int ntr) {
+  return D == 0 ? ntr : ntr / (G * S);
+}
+
 // Walk `ntr` trees (a multiple of S*G) of the chunk at `cb`, folding their
 // leaves into m in tree order.  Half-wave h walks trees [t0 + h*G, t0 +
 // (h+1)*G) of each group of S*G; with S = 2 only the lower half's m is the
 // candidate's margin.
+template <int D, int G, int S, typename After>
+__device__ __forceinline__ float walk_chunk_after(const char *cb, int ntr, const char *tile_lane,
+                                                  int h, float m, After after) {
+  constexpr uint32_t RB = record_bytes(D);
+  constexpr int GS = G * S;
+  auto fold = [&](const auto &A, const auto &B) {
+    if constexpr (G == 1) {
+      m = A.fold(m);
+      if constexpr (S == 2) m = A.fold_upper(m);
+    } else {
+      m = B.fold(A.fold(m));
+      if constexpr (S == 2) m = B.fold_upper(A.fold_upper(m));
+    }
+  };
+  if constexpr (D == 0) {  // ntr ragged slots
+    for (int i = 0; i < ntr; ++i) {
+      const char *slot = cb + (uint32_t)i * RB;
+      const SlotHead hd = slot_head(slot);
+      const uint32_t *roots = reinterpret_cast<const uint32_t *>(slot + 16) + h * G;
+      for (int t0 = 0; t0 < hd.ntrees; t0 += GS)
+        walk_group_ragged<G, S>(slot, roots + t0, hd.depth, hd.vbias, tile_lane, fold);
+      after(i);
+    }
+  } else {
+    for (int t0 = 0; t0 < ntr; t0 += GS) {
+      walk_group<D, G, S>(cb + (uint32_t)(t0 + h * G) * RB, tile_lane, fold);
+      after(t0 / GS);
+    }
+  }
+  return m;
+}
+
+// The same without a call between groups (the streamed chunks' walk).
 template <int D, int G, int S>
 __device__ __forceinline__ float walk_chunk(const char *cb, int ntr, const char *tile_lane,
                                             int h, float m) {
@@ -525,6 +565,32 @@ struct RowPrefetch {
   __device__ __forceinline__ void load(const WalkArgs &a, int64_t row, int h) {
 #pragma unroll
     for (int e = 0; e <= E; ++e) row_batch_load(a, row, h + e * S, v[e]);
+  }
+  template <int e>
+  __device__ __forceinline__ void load_batch(const WalkArgs &a, int64_t row, int h) {
+    row_batch_load(a, row, h + e * S, v[e]);
+  }
+  // Batch 0 is loaded before a walk; after group g of the walk, batch g+1:
+  // the loads of a round spread over the walk instead of reaching the memory
+  // path at once (all at the start of the walk, or later than one group
+  // ahead of the next round, measured slower).  load_rest() then loads the
+  // batches of a walk with fewer groups than batches.
+  __device__ __forceinline__ void load_after_group(const WalkArgs &a, int64_t row, int h, int g) {
+    static_assert(E <= 2, "extra batches beyond two");
+    if constexpr (E >= 1) {
+      if (g == 0) load_batch<1>(a, row, h);
+    }
+    if constexpr (E >= 2) {
+      if (g == 1) load_batch<2>(a, row, h);
+    }
+  }
+  __device__ __forceinline__ void load_rest(const WalkArgs &a, int64_t row, int h, int groups) {
+    if constexpr (E >= 1) {
+      if (groups < 1) load_batch<1>(a, row, h);
+    }
+    if constexpr (E >= 2) {
+      if (groups < 2) load_batch<2>(a, row, h);
+    }
   }
   // Write the prefetched batches into the tile, then load and write the lane
   // half's remaining batches.
@@ -639,17 +705,25 @@ __device__ __forceinline__ float walk_all(const WalkArgs &a, Stage<K, R> &s,
 // loop did, the compiler copied the prefetched rows at the merge and, to do
 // so, waited for every load in flight before each walk.  With S = 1 the
 // kernels are near their register limit and keep the single loop.
+// Resident ensembles with prefetched rows launch a kernel of their own
+// (RES), whose loop spreads the next round's row loads over the walk.  The
+// streamed kernel keeps its own resident loop (kResidentInline, not reached
+// from the launcher): built without it, the compiler laid out the streamed
+// loop so that the 16M-pool perf walk ran 2 % slower (measured three times).
 constexpr int kAny = 0;
 constexpr int kStreamed = 1;
-constexpr int kResident = 2;
+constexpr int kResident = 2;        // the resident kernel: loads spread over the walk
+constexpr int kResidentInline = 3;  // the same regime inside the streamed kernel
 
-template <int S, typename Rounds>
+template <int S, bool RES, typename Rounds>
 __device__ __forceinline__ void dispatch_rounds(const WalkArgs &a, Rounds &rounds) {
-  if constexpr (S == 2) {
+  if constexpr (RES) {
+    rounds(std::integral_constant<int, kResident>{});
+  } else if constexpr (S == 2) {
     if (!a.rowpf)
       rounds(std::integral_constant<int, kAny>{});
     else if (a.nchunks == 1)
-      rounds(std::integral_constant<int, kResident>{});
+      rounds(std::integral_constant<int, kResidentInline>{});
     else
       rounds(std::integral_constant<int, kStreamed>{});
   } else {
@@ -657,8 +731,13 @@ __device__ __forceinline__ void dispatch_rounds(const WalkArgs &a, Rounds &round
   }
 }
 
+// Launch the resident kernel (RES): S = 2, one chunk, rows prefetched.
+constexpr bool resident_launch(int S, const WalkArgs &a) {
+  return S == 2 && a.nchunks == 1 && a.rowpf;
+}
+
 // With S = 2 a kernel must leave room for two waves per SIMD (256 VGPRs).
-template <int D, int G, int S>
+template <int D, int G, int S, bool RES>
 __global__ void __launch_bounds__(kLanes *kMaxWaves) __attribute__((amdgpu_waves_per_eu(S, S)))
 validity_kernel(WalkArgs a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -679,7 +758,7 @@ validity_kernel(WalkArgs a) {
   stage_prime(a, RB, st);
   auto rounds = [&](auto mode) {
     constexpr int M = decltype(mode)::value;
-    constexpr int E = M == kResident ? row_extra_batches<S, kValiditySets, Geo<S>::kStageRegs>()
+    constexpr int E = M >= kResident ? row_extra_batches<S, kValiditySets, Geo<S>::kStageRegs>()
                                      : 0;
     RowPrefetch<S, E> pf;
     const bool pfr = M != kAny || a.rowpf;  // rows prefetched
@@ -687,25 +766,37 @@ validity_kernel(WalkArgs a) {
     for (int64_t tg = blockIdx.x; tg * W < ntiles; tg += gridDim.x) {
       const int64_t row = (tg * W + wave) * CPW + cl;
       const bool active = row < a.n;
+      const int64_t rn = ((tg + gridDim.x) * W + wave) * CPW + cl;
       if (pfr) {
         pf.commit(a, row, h, tile_lane);
-        pf.load(a, ((tg + gridDim.x) * W + wave) * CPW + cl, h);
+        if constexpr (M == kResident)
+          pf.template load_batch<0>(a, rn, h);
+        else
+          pf.load(a, rn, h);
       } else if (active && h == 0) {
         load_row<S>(a, row, tile_lane);
       }
       __syncthreads();
-      const float m = M == kResident ? walk_chunk<D, G, S>(st.cur, a.ntrees, tile_lane, h, a.base)
-                                     : walk_all<D, G, S>(a, st, tile_lane, h);
+      float m;
+      if constexpr (M == kResident) {
+        m = walk_chunk_after<D, G, S>(st.cur, a.ntrees, tile_lane, h, a.base,
+                                      [&](int g) { pf.load_after_group(a, rn, h, g); });
+        pf.load_rest(a, rn, h, walk_groups<D, G, S>(a.ntrees));
+      } else if constexpr (M == kResidentInline) {
+        m = walk_chunk<D, G, S>(st.cur, a.ntrees, tile_lane, h, a.base);
+      } else {
+        m = walk_all<D, G, S>(a, st, tile_lane, h);
+      }
       if (active && h == 0) {
         __builtin_nontemporal_store((uint8_t)((m > 0.0f) ? 1 : 0), a.valid_out + row);
         if (a.margin_out) __builtin_nontemporal_store(m, a.margin_out + row);
       }
     }
   };
-  dispatch_rounds<S>(a, rounds);
+  dispatch_rounds<S, RES>(a, rounds);
 }
 
-template <int D, int G, int S>
+template <int D, int G, int S, bool RES>
 __global__ void __launch_bounds__(kLanes *kMaxWaves) __attribute__((amdgpu_waves_per_eu(S, S)))
 perf_kernel(WalkArgs a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -767,7 +858,7 @@ perf_kernel(WalkArgs a) {
   };
   auto rounds = [&](auto mode) {  // see validity_kernel
     constexpr int M = decltype(mode)::value;
-    constexpr int E = M == kResident ? row_extra_batches<S, kPerfSets, Geo<S>::kStageRegs>() : 0;
+    constexpr int E = M >= kResident ? row_extra_batches<S, kPerfSets, Geo<S>::kStageRegs>() : 0;
     RowPrefetch<S, E> pf;
     const bool pfr = M != kAny || a.rowpf;  // rows prefetched
     int32_t row = next_rows();
@@ -779,14 +870,27 @@ perf_kernel(WalkArgs a) {
       else if (row >= 0 && h == 0)
         load_row<S>(a, row, tile_lane);
       const int32_t nrow = next_rows();  // ends with a barrier: the tiles are complete
-      if (pfr) pf.load(a, nrow, h);
-      const float m = M == kResident ? walk_chunk<D, G, S>(st.cur, a.ntrees, tile_lane, h, a.base)
-                                     : walk_all<D, G, S>(a, st, tile_lane, h);
+      if (pfr) {
+        if constexpr (M == kResident)
+          pf.template load_batch<0>(a, nrow, h);
+        else
+          pf.load(a, nrow, h);
+      }
+      float m;
+      if constexpr (M == kResident) {
+        m = walk_chunk_after<D, G, S>(st.cur, a.ntrees, tile_lane, h, a.base,
+                                      [&](int g) { pf.load_after_group(a, nrow, h, g); });
+        pf.load_rest(a, nrow, h, walk_groups<D, G, S>(a.ntrees));
+      } else if constexpr (M == kResidentInline) {
+        m = walk_chunk<D, G, S>(st.cur, a.ntrees, tile_lane, h, a.base);
+      } else {
+        m = walk_all<D, G, S>(a, st, tile_lane, h);
+      }
       if (row >= 0 && h == 0) __builtin_nontemporal_store(m, a.score_out + row);
       row = nrow;
     }
   };
-  dispatch_rounds<S>(a, rounds);
+  dispatch_rounds<S, RES>(a, rounds);
 }
 
 // Tree-parallel walk of a short row list (the second level): workgroup
@@ -876,23 +980,31 @@ constexpr bool group_allowed(int d, int g, int s) {
                  : (g == 1 || g == 2);
 }
 
+template <int D, int G, int S, bool RES>
+hipError_t launch_kernel(bool perf, const WalkPlan &p, const WalkArgs &a, hipStream_t s) {
+  const void *fn = perf ? reinterpret_cast<const void *>(&perf_kernel<D, G, S, RES>)
+                        : reinterpret_cast<const void *>(&validity_kernel<D, G, S, RES>);
+  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     (int)p.lds_bytes);
+  if (e != hipSuccess) return e;
+  dim3 grid(p.grid), block(p.waves * kLanes);
+  if (perf)
+    hipLaunchKernelGGL((perf_kernel<D, G, S, RES>), grid, block, p.lds_bytes, s, a);
+  else
+    hipLaunchKernelGGL((validity_kernel<D, G, S, RES>), grid, block, p.lds_bytes, s, a);
+  return hipGetLastError();
+}
+
 template <int D, int G, int S>
 hipError_t launch_dgs(bool perf, const WalkPlan &p, const WalkArgs &a, hipStream_t s) {
   // Chunks hold whole groups: every chunk's tree count, including the last
   // one's, is a multiple of the padding and hence of the group.
   static_assert((D == 0 ? kRaggedGroup : kTreePad) % (G * S) == 0,
                 "a walk group must divide the tree padding");
-  const void *fn = perf ? reinterpret_cast<const void *>(&perf_kernel<D, G, S>)
-                        : reinterpret_cast<const void *>(&validity_kernel<D, G, S>);
-  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                     (int)p.lds_bytes);
-  if (e != hipSuccess) return e;
-  dim3 grid(p.grid), block(p.waves * kLanes);
-  if (perf)
-    hipLaunchKernelGGL((perf_kernel<D, G, S>), grid, block, p.lds_bytes, s, a);
-  else
-    hipLaunchKernelGGL((validity_kernel<D, G, S>), grid, block, p.lds_bytes, s, a);
-  return hipGetLastError();
+  if constexpr (S == 2) {
+    if (resident_launch(S, a)) return launch_kernel<D, G, S, true>(perf, p, a, s);
+  }
+  return launch_kernel<D, G, S, false>(perf, p, a, s);
 }
 
 template <int D, int S>
