@@ -117,9 +117,10 @@ __device__ __forceinline__ void load_row(const WalkArgs &a, int64_t row, char *d
 // the row, lane half h taking lines h, h+S, ...; or, in the validity walk
 // with two lanes per candidate (P), a batch spans two lines of which lane
 // half h takes the vectors of parity h, so that one wave instruction
-// requests 32 lines (both halves' pieces of each line) instead of 64 (2.4 %
+// requests 32 lines (both halves' pieces of each line) instead of 64 (3 %
 // faster validity walk on the 16M pool; the perf walk, whose rows are
-// scattered over the pool, ran 0.4 % slower).  A wave never has requests for many lines of one row in
+// scattered over the pool, ran 0.4 % slower with it).  A wave never has
+// requests for many lines of one row in
 // flight at once, which was measured to fetch lines again and evict the
 // ensemble from L2.  The first batch of the next round's rows is fetched
 // while the current round is walked.  Loads are unconditional (a missing
