@@ -120,12 +120,11 @@ __device__ __forceinline__ void load_row(const WalkArgs &a, int64_t row, char *d
 // requests 32 lines (both halves' pieces of each line) instead of 64 (3 %
 // faster validity walk on the 16M pool; the perf walk, whose rows are
 // scattered over the pool, ran 0.4 % slower with it).  A wave never has
-// requests for many lines of one row in
-// flight at once, which was measured to fetch lines again and evict the
-// ensemble from L2.  The first batch of the next round's rows is fetched
-// while the current round is walked.  Loads are unconditional (a missing
-// row reads row 0, a short row repeats its last vector), so the compiler
-// knows how many are in flight.
+// requests for many lines of one row in flight at once, which was measured
+// to fetch lines again and evict the ensemble from L2.  The first batch of
+// the next round's rows is fetched while the current round is walked.
+// Loads are unconditional (a missing row reads row 0, a short row repeats
+// its last vector), so the compiler knows how many are in flight.
 constexpr int kRowVecs = 32;
 constexpr int kRowBatch = 8;
 
