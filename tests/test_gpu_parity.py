@@ -234,6 +234,20 @@ def test_resident_ensemble(monkeypatch, F, ld, trees):
     check_pipeline(V, P, X, 40, ld=ld)
 
 
+@pytest.mark.parametrize("F", [72, 96, 124, 128])
+def test_row_widths_two_lanes(monkeypatch, F):
+    """Two lanes per candidate with the ensemble streamed in several chunks:
+    row widths whose last line-batch is partial (the validity walk's halves
+    share each line, the perf walk's halves take alternate lines)."""
+    monkeypatch.setenv("ML2_WALK_SPLIT", "2")
+    K = F // 2
+    V = gen.perfect_ensemble(34, 1, 160, 6, F, K, 0.5)
+    P = gen.perfect_ensemble(34, 2, 120, 7, F, K, 0.1)
+    X = gen.features(34, 7001, F, K)
+    _note(f"row width F={F} (two lanes per candidate, streamed)")
+    check_pipeline(V, P, X, 64)
+
+
 def test_perf_without_mask():
     w = gen.WORKLOADS["tiny"]
     check_pipeline(w.validity(), w.perf(), w.features(), 64, perf_mask=False)
