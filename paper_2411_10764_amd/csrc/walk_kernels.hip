@@ -573,6 +573,57 @@ constexpr int row_extra_batches() {
   return S == 2 ? (K * R) / kRowBatch : 0;  // one lane per candidate: no room
 }
 
+// Lines shared by four lanes (P, S = 2): lanes (h, r, q) with h = lane bit
+// 5, r = lane bit 4 and q = lane bits 3..0 hold candidates q + 16r.  The four
+// lanes (h, r) of candidates q and q+16 load the four vectors 4j..4j+3 (one
+// 64-byte half) of a line, first of row q, then of row q+16 (lane (h, r)
+// takes vector 4j + 2r + h), so a wave instruction requests 16 half-lines;
+// one v_permlane16_swap per word then gives every lane the vectors of
+// parity h of its own row, as the paired layout expects (element k of a
+// batch = vector 2(k&3) + h of line k/4).
+__device__ __forceinline__ void quad_rows(int64_t row, int64_t &rx, int64_t &ry) {
+  const uint32_t lo = (uint32_t)(uint64_t)row, hi = (uint32_t)((uint64_t)row >> 32);
+  const auto l = __builtin_amdgcn_permlane16_swap(lo, lo, false, false);
+  const auto u = __builtin_amdgcn_permlane16_swap(hi, hi, false, false);
+  rx = (int64_t)(((uint64_t)u[0] << 32) | l[0]);  // the row of candidate q
+  ry = (int64_t)(((uint64_t)u[1] << 32) | l[1]);  // the row of candidate q + 16
+}
+
+__device__ __forceinline__ void row_batch_load_quad(const WalkArgs &a, int64_t rx, int64_t ry,
+                                                    int b, int h, f32x4 (&v)[kRowBatch]) {
+  const f32x4 *sx = row_src(a, rx);
+  const f32x4 *sy = row_src(a, ry);
+  const int last = a.F / 4 - 1;
+  const int r = (threadIdx.x >> 4) & 1;
+#pragma unroll
+  for (int l = 0; l < 2; ++l) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int q = min((2 * b + l) * kRowBatch + 4 * j + 2 * r + h, last);
+      v[4 * l + 2 * j] = sx[q];
+      v[4 * l + 2 * j + 1] = sy[q];
+    }
+  }
+}
+
+__device__ __forceinline__ void swap_rows16(f32x4 &x, f32x4 &y) {
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const auto t = __builtin_amdgcn_permlane16_swap(__float_as_uint(x[c]), __float_as_uint(y[c]),
+                                                    false, false);
+    x[c] = __uint_as_float(t[0]);
+    y[c] = __uint_as_float(t[1]);
+  }
+}
+
+__device__ __forceinline__ void quad_swap(f32x4 (&v)[kRowBatch]) {
+#pragma unroll
+  for (int l = 0; l < 2; ++l) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) swap_rows16(v[4 * l + 2 * j], v[4 * l + 2 * j + 1]);
+  }
+}
+
 template <int S, int E, bool P>
 struct RowPrefetch {
   f32x4 v[E + 1][kRowBatch];
@@ -581,12 +632,25 @@ struct RowPrefetch {
   __device__ __forceinline__ static int batch(int e, int h) { return P ? e : h + e * S; }
 
   __device__ __forceinline__ void load(const WalkArgs &a, int64_t row, int h) {
+    if constexpr (P) {
+      int64_t rx, ry;
+      quad_rows(row, rx, ry);
 #pragma unroll
-    for (int e = 0; e <= E; ++e) row_batch_load<P>(a, row, batch(e, h), h, v[e]);
+      for (int e = 0; e <= E; ++e) row_batch_load_quad(a, rx, ry, e, h, v[e]);
+    } else {
+#pragma unroll
+      for (int e = 0; e <= E; ++e) row_batch_load<P>(a, row, batch(e, h), h, v[e]);
+    }
   }
   template <int e>
   __device__ __forceinline__ void load_batch(const WalkArgs &a, int64_t row, int h) {
-    row_batch_load<P>(a, row, batch(e, h), h, v[e]);
+    if constexpr (P) {
+      int64_t rx, ry;
+      quad_rows(row, rx, ry);
+      row_batch_load_quad(a, rx, ry, e, h, v[e]);
+    } else {
+      row_batch_load<P>(a, row, batch(e, h), h, v[e]);
+    }
   }
   // Batch 0 is loaded before a walk; after group g of the walk, batch g+1:
   // the loads of a round spread over the walk instead of reaching the memory
@@ -612,18 +676,25 @@ struct RowPrefetch {
   }
   // Write the prefetched batches into the tile, then load and write the lane
   // half's remaining batches.
-  __device__ __forceinline__ void commit(const WalkArgs &a, int64_t row, int h,
-                                         char *dst) const {
-#pragma unroll
-    for (int e = 0; e <= E; ++e) row_batch_store<S, P>(a, batch(e, h), h, v[e], dst);
+  __device__ __forceinline__ void commit(const WalkArgs &a, int64_t row, int h, char *dst) {
     const int lines = (a.F / 4 + kRowBatch - 1) / kRowBatch;
     if constexpr (P) {
+#pragma unroll
+      for (int e = 0; e <= E; ++e) {
+        quad_swap(v[e]);
+        row_batch_store<S, P>(a, e, h, v[e], dst);
+      }
+      int64_t rx, ry;
+      quad_rows(row, rx, ry);
       for (int b = E + 1; 2 * b < lines; ++b) {
         f32x4 w[kRowBatch];
-        row_batch_load<P>(a, row, b, h, w);
+        row_batch_load_quad(a, rx, ry, b, h, w);
+        quad_swap(w);
         row_batch_store<S, P>(a, b, h, w, dst);
       }
     } else {
+#pragma unroll
+      for (int e = 0; e <= E; ++e) row_batch_store<S, P>(a, batch(e, h), h, v[e], dst);
       for (int b = h + (E + 1) * S; b < lines; b += S) {
         f32x4 w[kRowBatch];
         row_batch_load<P>(a, row, b, h, w);
