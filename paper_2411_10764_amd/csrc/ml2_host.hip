@@ -187,18 +187,22 @@ void pack_ragged(const std::vector<TreeView> &views, const std::vector<int> &dep
                  RaggedPack *out) {
   constexpr uint32_t CAP = ml2::kRaggedChunkBytes;
   constexpr int GRP = ml2::kRaggedGroup;
-  const uint32_t leaf_word0 = 0x7FFFFFu << 8;  // offset -1: the node itself
-  const uint32_t nan_bits = 0x7FC00000u;
+  const uint32_t leaf_word0 = 0x7FFFu << 16;  // offset -1: the node itself
+  auto bits = [](float v) {
+    uint32_t b;
+    memcpy(&b, &v, 4);
+    return b;
+  };
   size_t t = 0;
   int32_t tree_index = 0;
   while (t < views.size()) {
-    // choose the trees of this slot: header + roots + 12 bytes per node,
+    // choose the trees of this slot: header + roots + 8 bytes per node,
     // with room left for padding the tree count to a multiple of GRP
     size_t first = t, nodes = 0;
     auto need = [&](size_t ntrees, size_t nnodes) {
       const size_t ntr = (ntrees + GRP - 1) / GRP * GRP;
       const size_t head = (16 + 4 * ntr + 15) & ~(size_t)15;
-      return head + 12 * (nnodes + (ntr - ntrees));
+      return head + 8 * (nnodes + (ntr - ntrees));
     };
     while (t < views.size() && need(t + 1 - first, nodes + (size_t)views[t].size) <= CAP) {
       nodes += (size_t)views[t].size;
@@ -208,21 +212,18 @@ void pack_ragged(const std::vector<TreeView> &views, const std::vector<int> &dep
     const size_t ntr = (real + GRP - 1) / GRP * GRP;
     const size_t all_nodes = nodes + (ntr - real);
     const uint32_t head = (uint32_t)((16 + 4 * ntr + 15) & ~(size_t)15);
-    const uint32_t vals = head + 8u * (uint32_t)all_nodes;
     const size_t slot0 = out->bytes.size();
     out->bytes.resize(slot0 + CAP, 0);
     char *slot = out->bytes.data() + slot0;
     uint32_t *root = reinterpret_cast<uint32_t *>(slot + 16);
     uint2 *node = reinterpret_cast<uint2 *>(slot + head);
-    float *val = reinterpret_cast<float *>(slot + vals);
     int depth = 0;
     uint32_t next = 0;  // next free node index in the slot
     std::vector<int32_t> order;
     for (size_t i = 0; i < ntr; ++i) {
       root[i] = head / 8u + next;
       if (i >= real) {  // padding: one leaf of value -0.0
-        node[next] = make_uint2(leaf_word0, nan_bits);
-        val[next] = -0.0f;
+        node[next] = make_uint2(leaf_word0, bits(-0.0f));
         ++next;
         continue;
       }
@@ -244,23 +245,20 @@ void pack_ragged(const std::vector<TreeView> &views, const std::vector<int> &dep
         const int32_t o = order[k];
         const uint32_t j = next + (uint32_t)k;
         if (tv.left[o] == -1) {
-          node[j] = make_uint2(leaf_word0, nan_bits);
-          val[j] = tv.val[o];
+          node[j] = make_uint2(leaf_word0, bits(tv.val[o]));
         } else {
           const int32_t rel = newid[(size_t)tv.left[o]] - (int32_t)k;  // nodes, > 0
           const uint32_t dl = (tv.dl && tv.dl[o]) ? 1u : 0u;
           uint32_t tb;
           memcpy(&tb, &tv.thr[o], 4);
-          node[j] = make_uint2((dl << 31) | (((uint32_t)rel & 0x7FFFFFu) << 8) |
-                                   (uint32_t)tv.feat[o],
+          node[j] = make_uint2((dl << 31) | (((uint32_t)rel & 0x7FFFu) << 16) |
+                                   ((uint32_t)tv.feat[o] << 8),
                                tb);
-          val[j] = 0.0f;
         }
       }
       next += (uint32_t)order.size();
     }
-    // the value of the node with index u (8-byte units) is at byte vbias + 4u
-    const uint32_t hdr[4] = {(uint32_t)ntr, (uint32_t)depth, vals - head / 2, (uint32_t)tree_index};
+    const uint32_t hdr[4] = {(uint32_t)ntr, (uint32_t)depth, 0u, (uint32_t)tree_index};
     memcpy(slot, hdr, sizeof hdr);
     tree_index += (int32_t)ntr;
     if (depth > out->depth) out->depth = depth;

@@ -30,17 +30,18 @@ constexpr int kMaxPerfectDepth = 12;  // deeper ensembles use the ragged layout
 // missing values): the ensemble is cut into chunks of whole trees, each in a
 // fixed slot of kRaggedChunkBytes bytes:
 //   byte 0   uint4 {trees in the chunk (a multiple of kRaggedGroup), deepest
-//            path of those trees, vbias, global index of the chunk's first
-//            tree}; the value of the node with index u is at byte vbias + 4u
+//            path of those trees, 0, global index of the chunk's first tree}
 //   byte 16  uint32 root node index of each tree (node u at byte 8u of the
 //            slot)
 //   then 8-byte nodes, each tree breadth-first (siblings adjacent):
-//     word 0: bit 31 default-left, bits 30..8 signed offset in nodes from
-//             the node to its left child (the right child follows it),
-//             bits 7..0 split feature; word 1: threshold bits
-//     a leaf steps back onto itself: offset -1, threshold NaN, so x < t is
-//     false, it "goes right" to itself and a lockstep walk may run past it
-//   then one float per node (the leaf values; 0 for splits)
+//     split: word 0 bit 31 default-left, bits 30..16 signed offset in nodes
+//            from the node to its left child (the right child follows it;
+//            trees have at most 2041 nodes), bits 15..8 split feature,
+//            bits 7..0 zero (bits 15..0: the feature's byte offset in a
+//            256-byte-row tile); word 1 threshold bits
+//     leaf:  word 0 0x7FFF0000 (offset -1, feature 0), word 1 the leaf
+//            value; a walk treats a leaf as "go right", i.e. onto itself, so
+//            a lockstep walk may run past it
 // Trees padded onto a chunk are single leaves of value -0.0.
 constexpr uint32_t kRaggedChunkBytes = 24 * 1024;
 constexpr int kRaggedGroup = 4;

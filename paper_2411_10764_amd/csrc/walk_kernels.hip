@@ -312,8 +312,8 @@ struct Walks {
 // H walks of one half over a ragged chunk slot: u is the index of the
 // current 8-byte node in the slot.  One step: x < t goes left, a missing x
 // goes left where the node's default is left, else right; the right child
-// follows the left one (u <- u + offset + [right]), and a leaf steps onto
-// itself.
+// follows the left one (u <- u + offset + [right]), and a leaf (offset -1)
+// goes right, onto itself.  A leaf's second word is its value.
 template <int H, int S>
 struct RWalks {
   uint32_t u[H];
@@ -328,9 +328,9 @@ struct RWalks {
   __device__ __forceinline__ void read_features(const char *tile_lane) {
 #pragma unroll
     for (int g = 0; g < H; ++g) {
-      uint32_t f;
-      asm("v_bfe_u32 %0, %1, 0, 8" : "=v"(f) : "v"(nd[g].x));
-      x[g] = *reinterpret_cast<const float *>(tile_lane + (f << Geo<S>::kRowShift));
+      // bits 15..0 of word 0: the feature's offset in 256-byte tile rows
+      const uint32_t off = S == 1 ? (nd[g].x & 0xFFFFu) : (nd[g].x & 0xFFFFu) >> 1;
+      x[g] = *reinterpret_cast<const float *>(tile_lane + off);
     }
   }
   __device__ __forceinline__ void descend() {
@@ -338,15 +338,15 @@ struct RWalks {
     for (int g = 0; g < H; ++g) {
       const float t = __uint_as_float(nd[g].y);
       const bool missing_left = (int32_t)nd[g].x < 0 && __builtin_isnan(x[g]);
-      const bool right = !(x[g] < t) && !missing_left;
-      const int32_t off = (int32_t)(nd[g].x << 1) >> 9;  // bits 30..8, signed
+      const bool right = nd[g].x == kLeafWord || (!(x[g] < t) && !missing_left);
+      const int32_t off = (int32_t)(nd[g].x << 1) >> 17;  // bits 30..16, signed
       u[g] = u[g] + (uint32_t)off + (right ? 1u : 0u);
     }
   }
-  __device__ __forceinline__ void read_leaves(const char *slot, uint32_t vbias) {
+  // Once every walk is on a leaf, the nodes last read are the leaves.
+  __device__ __forceinline__ void take_leaves() {
 #pragma unroll
-    for (int g = 0; g < H; ++g)
-      leaf[g] = *reinterpret_cast<const float *>(slot + vbias + 4u * u[g]);
+    for (int g = 0; g < H; ++g) leaf[g] = __uint_as_float(nd[g].y);
   }
   // Every walk of this lane is on a leaf (whose first word is kLeafWord).
   __device__ __forceinline__ bool at_leaves() const {
@@ -365,21 +365,19 @@ struct RWalks {
     for (int g = 0; g < H; ++g) m = m + from_upper_half(leaf[g]);
     return m;
   }
-  static constexpr uint32_t kLeafWord = 0x7FFFFFu << 8;  // offset -1, feature 0
+  static constexpr uint32_t kLeafWord = 0x7FFFu << 16;  // offset -1, feature 0
 };
 
 // Ragged chunk slot header (see ml2_internal.h), read from LDS into scalars.
 struct SlotHead {
   int ntrees;
   int depth;
-  uint32_t vbias;
   int tree0;
 };
 
 __device__ __forceinline__ SlotHead slot_head(const char *slot) {
   const uint4 h = *reinterpret_cast<const uint4 *>(slot);
   return {__builtin_amdgcn_readfirstlane((int)h.x), __builtin_amdgcn_readfirstlane((int)h.y),
-          (uint32_t)__builtin_amdgcn_readfirstlane((int)h.z),
           __builtin_amdgcn_readfirstlane((int)h.w)};
 }
 
@@ -389,8 +387,8 @@ __device__ __forceinline__ SlotHead slot_head(const char *slot) {
 // themselves, so stopping at any point past that gives the same leaves.
 template <int G, int S, typename Done>
 __device__ __forceinline__ void walk_group_ragged(const char *slot, const uint32_t *roots,
-                                                  int depth, uint32_t vbias,
-                                                  const char *tile_lane, Done done) {
+                                                  int depth, const char *tile_lane,
+                                                  Done done) {
   if constexpr (G == 1) {
     RWalks<1, S> A;
     A.u[0] = roots[0];
@@ -401,7 +399,7 @@ __device__ __forceinline__ void walk_group_ragged(const char *slot, const uint32
       A.descend();
       A.read_nodes(slot);
     }
-    A.read_leaves(slot, vbias);
+    A.take_leaves();
     done(A, A);
   } else {
     constexpr int H = G / 2;
@@ -429,10 +427,97 @@ __device__ __forceinline__ void walk_group_ragged(const char *slot, const uint32
       B.read_nodes(slot);
       __builtin_amdgcn_sched_barrier(0);
     }
-    A.read_leaves(slot, vbias);
-    B.read_leaves(slot, vbias);
+    A.take_leaves();
+    B.take_leaves();
     done(A, B);
   }
+}
+
+// All groups of a ragged slot with one lane per candidate, each lane on its
+// own group: a lane whose G walks are all on leaves folds their values (the
+// leaves' second words, in tree order) and moves on to its next group while
+// the other lanes keep descending, so the wave waits for the lane with the
+// longest sum of group lengths instead of, group by group, for the longest
+// path of any lane.  The roots of a lane's next group are read at every
+// step, so a move never waits for LDS.  Every lane is done after at most
+// (groups) x (depth + 1) steps; the loop stops a little past that at the
+// latest.
+template <int G>
+__device__ __forceinline__ float walk_slot_lanes(const char *slot, int ntr, int depth,
+                                                 const char *tile_lane, float m) {
+  constexpr int H = G == 1 ? 1 : G / 2;
+  using RootVec = std::conditional_t<G == 4, uint4, std::conditional_t<G == 2, uint2, uint32_t>>;
+  const uint32_t *roots = reinterpret_cast<const uint32_t *>(slot + 16);
+  auto load_roots = [&](int t, uint32_t (&r)[G]) {  // t: a multiple of G, at most ntr + G
+    const RootVec v = *reinterpret_cast<const RootVec *>(roots + t);
+    if constexpr (G == 4) {
+      r[0] = v.x;
+      r[1] = v.y;
+      r[2] = v.z;
+      r[3] = v.w;
+    } else if constexpr (G == 2) {
+      r[0] = v.x;
+      r[1] = v.y;
+    } else {
+      r[0] = v;
+    }
+  };
+  RWalks<H, 1> A, B;
+  uint32_t nxt[G];
+  load_roots(0, nxt);
+#pragma unroll
+  for (int g = 0; g < H; ++g) {
+    A.u[g] = nxt[g];
+    if constexpr (G > 1) B.u[g] = nxt[H + g];
+  }
+  A.read_nodes(slot);
+  if constexpr (G > 1) B.read_nodes(slot);
+  // t: the lane's next group (its current group is the one before; ntr + G
+  // once every group is done).  Reading the roots of a group past the last
+  // reads node words of the slot, which a finished lane never uses.
+  int t = G;
+  load_roots(t, nxt);
+  __builtin_amdgcn_sched_barrier(0);
+  // The only exit is at the bottom: an early exit made the compiler wait
+  // for every LDS read in flight at the top of each step.
+  const int cap = (ntr / G) * (depth + 2) + 2;
+  int it = 0;
+  bool go = true;
+  while (go) {
+    A.read_features(tile_lane);
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (G > 1) B.read_features(tile_lane);
+    __builtin_amdgcn_sched_barrier(0);
+    const bool fin = t > ntr;
+    bool leaves = A.at_leaves();
+    if constexpr (G > 1) leaves = leaves && B.at_leaves();
+    const bool sw = !fin && leaves;
+    float fm = m;
+#pragma unroll
+    for (int g = 0; g < H; ++g) fm = fm + __uint_as_float(A.nd[g].y);
+    if constexpr (G > 1) {
+#pragma unroll
+      for (int g = 0; g < H; ++g) fm = fm + __uint_as_float(B.nd[g].y);
+    }
+    m = sw ? fm : m;
+    const bool mv = sw && t < ntr;
+    t += sw ? G : 0;
+    A.descend();
+#pragma unroll
+    for (int g = 0; g < H; ++g) A.u[g] = mv ? nxt[g] : A.u[g];
+    A.read_nodes(slot);
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (G > 1) {
+      B.descend();
+#pragma unroll
+      for (int g = 0; g < H; ++g) B.u[g] = mv ? nxt[H + g] : B.u[g];
+      B.read_nodes(slot);
+    }
+    load_roots(t, nxt);
+    __builtin_amdgcn_sched_barrier(0);
+    go = !__all(t > ntr) && ++it < cap;
+  }
+  return m;
 }
 
 // One group: half-wave h walks the G trees of records starting at `rec`
@@ -508,9 +593,13 @@ __device__ __forceinline__ float walk_chunk_after(const char *cb, int ntr, const
     for (int i = 0; i < ntr; ++i) {
       const char *slot = cb + (uint32_t)i * RB;
       const SlotHead hd = slot_head(slot);
-      const uint32_t *roots = reinterpret_cast<const uint32_t *>(slot + 16) + h * G;
-      for (int t0 = 0; t0 < hd.ntrees; t0 += GS)
-        walk_group_ragged<G, S>(slot, roots + t0, hd.depth, hd.vbias, tile_lane, fold);
+      if constexpr (S == 1) {
+        m = walk_slot_lanes<G>(slot, hd.ntrees, hd.depth, tile_lane, m);
+      } else {
+        const uint32_t *roots = reinterpret_cast<const uint32_t *>(slot + 16) + h * G;
+        for (int t0 = 0; t0 < hd.ntrees; t0 += GS)
+          walk_group_ragged<G, S>(slot, roots + t0, hd.depth, tile_lane, fold);
+      }
       after(i);
     }
   } else {
@@ -541,9 +630,13 @@ __device__ __forceinline__ float walk_chunk(const char *cb, int ntr, const char 
     for (int i = 0; i < ntr; ++i) {
       const char *slot = cb + (uint32_t)i * RB;
       const SlotHead hd = slot_head(slot);
-      const uint32_t *roots = reinterpret_cast<const uint32_t *>(slot + 16) + h * G;
-      for (int t0 = 0; t0 < hd.ntrees; t0 += GS)
-        walk_group_ragged<G, S>(slot, roots + t0, hd.depth, hd.vbias, tile_lane, fold);
+      if constexpr (S == 1) {
+        m = walk_slot_lanes<G>(slot, hd.ntrees, hd.depth, tile_lane, m);
+      } else {
+        const uint32_t *roots = reinterpret_cast<const uint32_t *>(slot + 16) + h * G;
+        for (int t0 = 0; t0 < hd.ntrees; t0 += GS)
+          walk_group_ragged<G, S>(slot, roots + t0, hd.depth, tile_lane, fold);
+      }
     }
   } else {
     for (int t0 = 0; t0 < ntr; t0 += GS)
@@ -1038,7 +1131,7 @@ __global__ void __launch_bounds__(kLanes * 4) leaves_kernel(WalkArgs a) {
       const SlotHead hd = slot_head(slot);
       const uint32_t *roots = reinterpret_cast<const uint32_t *>(slot + 16);
       for (int g0 = 0; g0 < hd.ntrees; g0 += G)
-        walk_group_ragged<G, 1>(slot, roots + g0, hd.depth, hd.vbias, tile_lane,
+        walk_group_ragged<G, 1>(slot, roots + g0, hd.depth, tile_lane,
                                 [&](const auto &A, const auto &B) { store(hd.tree0 + g0, A, B); });
     }
   } else {

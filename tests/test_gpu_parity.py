@@ -390,3 +390,53 @@ def test_full_size_sampled(name):
     _note(f"{name}: invalid fraction {1 - n_valid / w.n:.4f}; sampled rows exact; top-{w.k} ok")
     v.free()
     p.free()
+
+
+# ---- one GPU's share and the merge of shards ---------------------------------------
+
+@pytest.mark.slow
+def test_shard_merge_matches_whole():
+    """One GPU's share of the 16M-candidate pool with eight GPUs (2^21 rows x
+    128, the same ensembles), split into eight uneven contiguous pseudo-shards.
+    Each shard runs the whole path on its rows; the union of the shards'
+    top-k lists, selected again with ml2_filter_topk, must equal the top-k of
+    the undivided share bit for bit (indices and scores), because each
+    candidate's scores do not depend on the shard and the key order (score
+    descending, index ascending) is the same in every shard."""
+    w = gen.WORKLOADS["roofline"]
+    n, G, k = 1 << 21, 8, w.k
+    _note(f"shard merge: {n} x {w.F} rows, {G} pseudo-shards, k = {k}")
+    X = gen.features(w.seed, n, w.F, w.K)
+    Xd = torch.from_numpy(X).to(DEV)
+    v, p = ml2.ml2_load_ensemble(w.validity()), ml2.ml2_load_ensemble(w.perf())
+    whole = ml2.Pipeline(v, p, n, k, device=DEV)
+    whole.run(Xd)
+    rng = np.random.default_rng(11)
+    cuts = np.sort(rng.choice(np.arange(1, n), G - 1, replace=False))
+    bounds = np.concatenate([[0], cuts, [n]]).astype(np.int64)
+    cat_score = torch.full((G * k,), -math.inf, dtype=torch.float32, device=DEV)
+    cat_valid = torch.zeros(G * k, dtype=torch.uint8, device=DEV)
+    cat_idx = torch.full((G * k,), -1, dtype=torch.int64, device=DEV)
+    for g in range(G):
+        r0, r1 = int(bounds[g]), int(bounds[g + 1])
+        part = ml2.Pipeline(v, p, r1 - r0, k, device=DEV)
+        part.run(Xd[r0:r1])
+        m = part.num[0]
+        sl = slice(g * k, (g + 1) * k)
+        used = torch.arange(k, device=DEV) < m
+        cat_score[sl] = torch.where(used, part.top[:k], cat_score[sl])
+        cat_valid[sl] = used.to(torch.uint8)
+        cat_idx[sl] = torch.where(used, part.idx[:k].to(torch.int64) + r0, cat_idx[sl])
+    merged = ml2.Pipeline(v, p, G * k, k, device=DEV)
+    ml2.ml2_filter_topk(cat_valid, cat_score, k, merged.idx, merged.top, merged.num,
+                        merged.ws, merged.ws_bytes, G * k)
+    torch.cuda.synchronize()
+    num = int(whole.num.item())
+    assert int(merged.num.item()) == num == k
+    got_idx = cat_idx[merged.idx[:num].to(torch.int64)].cpu().numpy()
+    assert np.array_equal(got_idx, whole.idx[:num].cpu().numpy().astype(np.int64))
+    assert np.array_equal(merged.top[:num].cpu().numpy().view(np.uint32),
+                          whole.top[:num].cpu().numpy().view(np.uint32))
+    _note(f"shard merge: shards {np.diff(bounds).tolist()}; merged top-{k} identical")
+    v.free()
+    p.free()

@@ -71,16 +71,20 @@ def test_paper_shaped_pipeline_with_missing_values():
     check_rerank(A, X, rows, 100)
 
 
-@pytest.mark.parametrize("split,waves,nbuf", [(1, 4, 1), (1, 8, 1), (2, 8, 1), (1, 4, 2),
-                                              (2, 4, 1), (1, 2, 1)])
-def test_ragged_plans(monkeypatch, split, waves, nbuf):
-    for key, val in (("SPLIT", split), ("WAVES", waves), ("NBUF", nbuf)):
-        monkeypatch.setenv(f"ML2_WALK_{key}", str(val))
+@pytest.mark.parametrize("split,waves,nbuf,group", [
+    (1, 4, 1, 0), (1, 8, 1, 0), (2, 8, 1, 0), (1, 4, 2, 0), (2, 4, 1, 0), (1, 2, 1, 0),
+    (1, 8, 1, 1), (1, 8, 1, 2), (1, 4, 2, 4), (2, 8, 1, 1), (2, 8, 1, 2)])
+def test_ragged_plans(monkeypatch, split, waves, nbuf, group):
+    """Launch shapes of the ragged walks; group 0 leaves the trees per lane
+    to the planner."""
+    for key, val in (("SPLIT", split), ("WAVES", waves), ("NBUF", nbuf), ("GROUP", group)):
+        if val:
+            monkeypatch.setenv(f"ML2_WALK_{key}", str(val))
     n, F, K = 3000, 40, 20
     V = gen.ragged_ensemble(63, 1, 60, 9, F, K, 0.5, base_score=0.2, max_nodes=300)
     P = gen.ragged_ensemble(63, 2, 90, 14, F, K, 0.1, max_nodes=300)
     X = gen.features(63, n, F, K, missing=0.2)
-    _note(f"ragged plan S={split} W={waves} nbuf={nbuf}")
+    _note(f"ragged plan S={split} W={waves} nbuf={nbuf} G={group}")
     check_pipeline(V, P, X, 50)
 
 
