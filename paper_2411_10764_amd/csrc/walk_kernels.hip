@@ -1368,7 +1368,8 @@ bool try_plan(const Forest &f, int64_t n_work, int cu_count, int S, int W, int m
 // (two per SIMD), with one lane per candidate where eight full tiles fit
 // (twice the candidates per pass over the ensemble), else two; then one lane
 // per candidate with four waves in the order register staging, two buffers,
-// synchronous copy; then fewer waves.  Larger G first within each.  ML2_WALK_SPLIT /
+// synchronous copy; then fewer waves.  Larger G first within each (ragged
+// trees with one lane per candidate: smaller G first).  ML2_WALK_SPLIT /
 // ML2_WALK_GROUP / ML2_WALK_WAVES / ML2_WALK_NBUF / ML2_WALK_CHUNK override
 // the choice (tuning sweeps); overrides that do not fit are ignored.
 bool plan_walk(const Forest &f, int64_t n_work, int cu_count, WalkPlan *p, const char **why) {
@@ -1378,6 +1379,10 @@ bool plan_walk(const Forest &f, int64_t n_work, int cu_count, WalkPlan *p, const
   const int want_b = env_int("ML2_WALK_NBUF", 0);
   const int want_c = env_int("ML2_WALK_CHUNK", 0);
   const int groups[5] = {16, 8, 4, 2, 1};
+  // ragged trees with one lane per candidate: one tree per lane first (each
+  // lane then moves to its next tree as soon as its walk is on a leaf, and
+  // no walk waits for a longer one of its lane)
+  const int ragged_groups[5] = {1, 2, 4, 0, 0};
   struct Shape { int s, w; };
   const Shape shapes[] = {{1, 8}, {2, 8}, {1, 4}, {2, 4}, {1, 2}, {1, 1}};
   for (int pass = 0; pass < 2; ++pass) {  // pass 0 honours the overrides
@@ -1389,7 +1394,8 @@ bool plan_walk(const Forest &f, int64_t n_work, int cu_count, WalkPlan *p, const
       }
       for (int mode = 0; mode < 3; ++mode) {
         if (pass == 0 && want_b && want_b != (mode == 1 ? 2 : 1)) continue;
-        for (int G : groups) {
+        for (int G : (f.ragged && S == 1) ? ragged_groups : groups) {
+          if (G == 0) break;
           if (pass == 0 && want_g && group_allowed(f.ragged ? 0 : f.depth, want_g, S) &&
               G != want_g)
             continue;
