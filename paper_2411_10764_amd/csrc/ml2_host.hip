@@ -199,10 +199,11 @@ void pack_ragged(const std::vector<TreeView> &views, const std::vector<int> &dep
     // choose the trees of this slot: header + roots + 8 bytes per node,
     // with room left for padding the tree count to a multiple of GRP
     size_t first = t, nodes = 0;
+    // (two more root entries and one more node: the sentinel)
     auto need = [&](size_t ntrees, size_t nnodes) {
       const size_t ntr = (ntrees + GRP - 1) / GRP * GRP;
-      const size_t head = (16 + 4 * ntr + 15) & ~(size_t)15;
-      return head + 8 * (nnodes + (ntr - ntrees));
+      const size_t head = (16 + 4 * (ntr + 2) + 15) & ~(size_t)15;
+      return head + 8 * (nnodes + (ntr - ntrees) + 1);
     };
     while (t < views.size() && need(t + 1 - first, nodes + (size_t)views[t].size) <= CAP) {
       nodes += (size_t)views[t].size;
@@ -211,7 +212,7 @@ void pack_ragged(const std::vector<TreeView> &views, const std::vector<int> &dep
     const size_t real = t - first;
     const size_t ntr = (real + GRP - 1) / GRP * GRP;
     const size_t all_nodes = nodes + (ntr - real);
-    const uint32_t head = (uint32_t)((16 + 4 * ntr + 15) & ~(size_t)15);
+    const uint32_t head = (uint32_t)((16 + 4 * (ntr + 2) + 15) & ~(size_t)15);
     const size_t slot0 = out->bytes.size();
     out->bytes.resize(slot0 + CAP, 0);
     char *slot = out->bytes.data() + slot0;
@@ -258,6 +259,12 @@ void pack_ragged(const std::vector<TreeView> &views, const std::vector<int> &dep
       }
       next += (uint32_t)order.size();
     }
+    // the sentinel: a leaf of value -0.0 that the two entries after the last
+    // root point to (a walk past its last tree moves onto it; adding -0.0
+    // changes no float)
+    node[next] = make_uint2(leaf_word0, bits(-0.0f));
+    root[ntr] = root[ntr + 1] = head / 8u + next;
+    ++next;
     const uint32_t hdr[4] = {(uint32_t)ntr, (uint32_t)depth, 0u, (uint32_t)tree_index};
     memcpy(slot, hdr, sizeof hdr);
     tree_index += (int32_t)ntr;

@@ -32,7 +32,7 @@ constexpr int kMaxPerfectDepth = 12;  // deeper ensembles use the ragged layout
 //   byte 0   uint4 {trees in the chunk (a multiple of kRaggedGroup), deepest
 //            path of those trees, 0, global index of the chunk's first tree}
 //   byte 16  uint32 root node index of each tree (node u at byte 8u of the
-//            slot)
+//            slot), then two entries that point to the sentinel
 //   then 8-byte nodes, each tree breadth-first (siblings adjacent):
 //     split: word 0 bit 31 default-left, bits 30..16 signed offset in nodes
 //            from the node to its left child (the right child follows it;
@@ -42,7 +42,8 @@ constexpr int kMaxPerfectDepth = 12;  // deeper ensembles use the ragged layout
 //     leaf:  word 0 0x7FFF0000 (offset -1, feature 0), word 1 the leaf
 //            value; a walk treats a leaf as "go right", i.e. onto itself, so
 //            a lockstep walk may run past it
-// Trees padded onto a chunk are single leaves of value -0.0.
+// Trees padded onto a chunk are single leaves of value -0.0; the sentinel,
+// after the last tree, is one more such leaf.
 constexpr uint32_t kRaggedChunkBytes = 24 * 1024;
 constexpr int kRaggedGroup = 4;
 constexpr size_t kTreeSlack = 128 * 1024;  // readable zero bytes after the tree table

@@ -520,6 +520,56 @@ __device__ __forceinline__ float walk_slot_lanes(const char *slot, int ntr, int 
   return m;
 }
 
+// A ragged slot with one lane per candidate and one tree per lane: a walk on
+// a leaf adds the leaf's value and, in the same step, moves on to the root
+// of the lane's next tree, so no lane waits for another's path.  Past its
+// last tree a lane moves onto the slot's sentinel (two root entries after
+// the last tree, a leaf of value -0.0), and adding -0.0 leaves every float
+// unchanged, so a finished lane needs no test of its own.  The roots entry
+// of the next tree is read at every step.  Every lane is done after at most
+// (trees) x (depth + 1) steps; the loop stops a little past that at the
+// latest.
+__device__ __forceinline__ float walk_slot_single(const char *slot, int ntr, int depth,
+                                                  const char *tile_lane, float m) {
+  const uint32_t *roots = reinterpret_cast<const uint32_t *>(slot + 16);
+  RWalks<1, 1> A;
+  A.u[0] = roots[0];
+  A.read_nodes(slot);
+  int t = 1;  // the roots entry of the lane's next tree (ntr + 1: done)
+  // read after the node, as the loop does (not folded into the read above),
+  // so that the loop starts with the reads in flight that it ends with
+  int t0 = 1;
+  asm volatile("" : "+v"(t0));
+  uint32_t nxt = roots[t0];
+  __builtin_amdgcn_sched_barrier(0);
+  const int cap = ntr * (depth + 2) + 4;
+  int it = 0;
+  bool go = true;
+  while (go) {
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      A.read_features(tile_lane);
+      __builtin_amdgcn_sched_barrier(0);
+      const uint32_t w0 = A.nd[0].x;
+      const bool leaf = w0 == RWalks<1, 1>::kLeafWord;
+      m = m + (leaf ? __uint_as_float(A.nd[0].y) : -0.0f);
+      const bool missing_left = (int32_t)w0 < 0 && __builtin_isnan(A.x[0]);
+      const bool right = !(A.x[0] < __uint_as_float(A.nd[0].y)) && !missing_left;
+      const int32_t off = (int32_t)(w0 << 1) >> 17;  // bits 30..16, signed
+      uint32_t un = A.u[0] + (uint32_t)off + (right ? 1u : 0u);
+      asm volatile("" : "+v"(un));  // computed by every lane: no branch
+      A.u[0] = leaf ? nxt : un;
+      t = min(t + (leaf ? 1 : 0), ntr + 1);
+      A.read_nodes(slot);
+      nxt = roots[t];
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    it += 2;
+    go = !__all(t > ntr) && it < cap;
+  }
+  return m;
+}
+
 // One group: half-wave h walks the G trees of records starting at `rec`
 // (two halves of H = G/2 offset by half a level), then `done(A, B)` gets the
 // leaves (A: the first H trees, B: the next H; with G == 1 only A).
@@ -593,7 +643,9 @@ __device__ __forceinline__ float walk_chunk_after(const char *cb, int ntr, const
     for (int i = 0; i < ntr; ++i) {
       const char *slot = cb + (uint32_t)i * RB;
       const SlotHead hd = slot_head(slot);
-      if constexpr (S == 1) {
+      if constexpr (S == 1 && G == 1) {
+        m = walk_slot_single(slot, hd.ntrees, hd.depth, tile_lane, m);
+      } else if constexpr (S == 1) {
         m = walk_slot_lanes<G>(slot, hd.ntrees, hd.depth, tile_lane, m);
       } else {
         const uint32_t *roots = reinterpret_cast<const uint32_t *>(slot + 16) + h * G;
@@ -630,7 +682,9 @@ __device__ __forceinline__ float walk_chunk(const char *cb, int ntr, const char 
     for (int i = 0; i < ntr; ++i) {
       const char *slot = cb + (uint32_t)i * RB;
       const SlotHead hd = slot_head(slot);
-      if constexpr (S == 1) {
+      if constexpr (S == 1 && G == 1) {
+        m = walk_slot_single(slot, hd.ntrees, hd.depth, tile_lane, m);
+      } else if constexpr (S == 1) {
         m = walk_slot_lanes<G>(slot, hd.ntrees, hd.depth, tile_lane, m);
       } else {
         const uint32_t *roots = reinterpret_cast<const uint32_t *>(slot + 16) + h * G;
