@@ -526,9 +526,10 @@ __device__ __forceinline__ float walk_slot_lanes(const char *slot, int ntr, int 
 // last tree a lane moves onto the slot's sentinel (two root entries after
 // the last tree, a leaf of value -0.0), and adding -0.0 leaves every float
 // unchanged, so a finished lane needs no test of its own.  The roots entry
-// of the next tree is read at every step.  Every lane is done after at most
-// (trees) x (depth + 1) steps; the loop stops a little past that at the
-// latest.
+// of the next tree is read at every step.  The loop runs eight steps per
+// trip (one exit test per trip; a finished lane's extra steps change
+// nothing).  Every lane is done after at most (trees) x (depth + 1) steps;
+// the loop stops a little past that at the latest.
 __device__ __forceinline__ float walk_slot_single(const char *slot, int ntr, int depth,
                                                   const char *tile_lane, float m) {
   const uint32_t *roots = reinterpret_cast<const uint32_t *>(slot + 16);
@@ -547,7 +548,7 @@ __device__ __forceinline__ float walk_slot_single(const char *slot, int ntr, int
   bool go = true;
   while (go) {
 #pragma unroll
-    for (int k = 0; k < 2; ++k) {
+    for (int k = 0; k < 8; ++k) {
       A.read_features(tile_lane);
       __builtin_amdgcn_sched_barrier(0);
       const uint32_t w0 = A.nd[0].x;
@@ -564,7 +565,7 @@ __device__ __forceinline__ float walk_slot_single(const char *slot, int ntr, int
       nxt = roots[t];
       __builtin_amdgcn_sched_barrier(0);
     }
-    it += 2;
+    it += 8;
     go = !__all(t > ntr) && it < cap;
   }
   return m;
