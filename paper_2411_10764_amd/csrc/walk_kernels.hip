@@ -389,15 +389,21 @@ template <int G, int S, typename Done>
 __device__ __forceinline__ void walk_group_ragged(const char *slot, const uint32_t *roots,
                                                   int depth, const char *tile_lane,
                                                   Done done) {
+  // Loops whose only exit is at the bottom (an early exit made the compiler
+  // wait for every LDS read in flight at the top of each step): a step whose
+  // walks are all on leaves is still taken, as leaves step onto themselves.
   if constexpr (G == 1) {
     RWalks<1, S> A;
     A.u[0] = roots[0];
     A.read_nodes(slot);
-    for (int l = 0; l < depth; ++l) {
+    int l = 0;
+    bool go = depth > 0;
+    while (go) {
       A.read_features(tile_lane);
-      if (__all(A.at_leaves())) break;
+      const bool all = __all(A.at_leaves());
       A.descend();
       A.read_nodes(slot);
+      go = !all && ++l < depth;
     }
     A.take_leaves();
     done(A, A);
@@ -412,20 +418,23 @@ __device__ __forceinline__ void walk_group_ragged(const char *slot, const uint32
     A.read_nodes(slot);
     B.read_nodes(slot);
     __builtin_amdgcn_sched_barrier(0);
-    for (int l = 0; l < depth; ++l) {
+    int l = 0;
+    bool go = depth > 0;
+    while (go) {
       // the exit test follows the feature reads, so that it does not hold
       // them back until every node read has landed
       A.read_features(tile_lane);
       __builtin_amdgcn_sched_barrier(0);
       B.read_features(tile_lane);
       __builtin_amdgcn_sched_barrier(0);
-      if (__all(A.at_leaves() && B.at_leaves())) break;
+      const bool all = __all(A.at_leaves() && B.at_leaves());
       A.descend();
       A.read_nodes(slot);
       __builtin_amdgcn_sched_barrier(0);
       B.descend();
       B.read_nodes(slot);
       __builtin_amdgcn_sched_barrier(0);
+      go = !all && ++l < depth;
     }
     A.take_leaves();
     B.take_leaves();

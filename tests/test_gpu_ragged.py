@@ -88,6 +88,25 @@ def test_ragged_plans(monkeypatch, split, waves, nbuf, group):
     check_pipeline(V, P, X, 50)
 
 
+@pytest.mark.parametrize("split,group", [(0, 0), (1, 2), (1, 4), (2, 0), (2, 1)])
+def test_ragged_shallow_trees(monkeypatch, split, group):
+    """Shallow trees (one to three splits; walks that end after a step or
+    two, lanes that run through a slot's trees in a few steps, single-leaf
+    padding trees after P's 37), V a slot of exactly four trees; the default
+    plan, groups of two and four trees per lane, and two lanes per
+    candidate."""
+    for key, val in (("SPLIT", split), ("GROUP", group)):
+        if val:
+            monkeypatch.setenv(f"ML2_WALK_{key}", str(val))
+    n, F, K = 2500, 24, 12
+    V = gen.ragged_ensemble(66, 1, 4, 3, F, K, 0.5, base_score=0.1, p_split=0.3)
+    P = gen.ragged_ensemble(66, 2, 37, 6, F, K, 0.1, p_split=0.3, decay=0.5)
+    X = gen.features(66, n, F, K, missing=0.1)
+    _note(f"shallow ragged S={split} G={group}: P trees of "
+          f"{int(np.diff(P.offsets).max())} nodes at most")
+    check_pipeline(V, P, X, 30)
+
+
 def test_forced_ragged_layout_on_perfect_trees(monkeypatch):
     """Perfect trees packed into ragged slots give the same results."""
     monkeypatch.setenv("ML2_LAYOUT", "ragged")
