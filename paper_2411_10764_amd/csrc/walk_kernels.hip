@@ -781,15 +781,18 @@ __device__ __forceinline__ void quad_swap(f32x4 (&v)[kRowBatch]) {
   }
 }
 
-template <int S, int E, bool P>
+// P: the lane halves take their halves of the same lines (paired layout);
+// Q: with P, the lines shared by four lanes (quad loads).
+template <int S, int E, bool P, bool Q = P>
 struct RowPrefetch {
+  static_assert(P || !Q, "quad loads fill the paired layout");
   f32x4 v[E + 1][kRowBatch];
 
   // the batch index of prefetched batch e of lane half h
   __device__ __forceinline__ static int batch(int e, int h) { return P ? e : h + e * S; }
 
   __device__ __forceinline__ void load(const WalkArgs &a, int64_t row, int h) {
-    if constexpr (P) {
+    if constexpr (Q) {
       int64_t rx, ry;
       quad_rows(row, rx, ry);
 #pragma unroll
@@ -801,7 +804,7 @@ struct RowPrefetch {
   }
   template <int e>
   __device__ __forceinline__ void load_batch(const WalkArgs &a, int64_t row, int h) {
-    if constexpr (P) {
+    if constexpr (Q) {
       int64_t rx, ry;
       quad_rows(row, rx, ry);
       row_batch_load_quad(a, rx, ry, e, h, v[e]);
@@ -835,7 +838,7 @@ struct RowPrefetch {
   // half's remaining batches.
   __device__ __forceinline__ void commit(const WalkArgs &a, int64_t row, int h, char *dst) {
     const int lines = (a.F / 4 + kRowBatch - 1) / kRowBatch;
-    if constexpr (P) {
+    if constexpr (Q) {
 #pragma unroll
       for (int e = 0; e <= E; ++e) {
         quad_swap(v[e]);
@@ -847,6 +850,14 @@ struct RowPrefetch {
         f32x4 w[kRowBatch];
         row_batch_load_quad(a, rx, ry, b, h, w);
         quad_swap(w);
+        row_batch_store<S, P>(a, b, h, w, dst);
+      }
+    } else if constexpr (P) {
+#pragma unroll
+      for (int e = 0; e <= E; ++e) row_batch_store<S, P>(a, e, h, v[e], dst);
+      for (int b = E + 1; 2 * b < lines; ++b) {
+        f32x4 w[kRowBatch];
+        row_batch_load<P>(a, row, b, h, w);
         row_batch_store<S, P>(a, b, h, w, dst);
       }
     } else {
@@ -1014,7 +1025,10 @@ validity_kernel(WalkArgs a) {
     constexpr int M = decltype(mode)::value;
     constexpr int E = M >= kResident ? row_extra_batches<S, kValiditySets, Geo<S>::kStageRegs>()
                                      : 0;
-    RowPrefetch<S, E, S == 2> pf;
+    // lines shared by four lanes in the streamed kernel only (validity
+    // 8.56 -> 8.31 ms on the 16M pool; the resident kernel of the HBM-bound
+    // diagnostic ran 8 % slower with them)
+    RowPrefetch<S, E, S == 2, S == 2 && !RES> pf;
     const bool pfr = M != kAny || a.rowpf;  // rows prefetched
     if (pfr) pf.load(a, ((int64_t)blockIdx.x * W + wave) * CPW + cl, h);
     for (int64_t tg = blockIdx.x; tg * W < ntiles; tg += gridDim.x) {
