@@ -963,6 +963,36 @@ __device__ __forceinline__ float walk_all(const WalkArgs &a, Stage<K, R> &s,
   return m;
 }
 
+// walk_all, calling after() once the first chunk is walked (streamed
+// ensembles, register staging: the streamed validity walk loads its second
+// row batch for the next round there).
+template <int D, int G, int S, int K, int R, typename After>
+__device__ __forceinline__ float walk_all_after(const WalkArgs &a, Stage<K, R> &s,
+                                                const char *tile_lane, int h, After after) {
+  constexpr uint32_t RB = record_bytes(D);
+  if (!a.regstage || a.nchunks == 1) {  // not the case the launcher sends here
+    const float m = walk_all<D, G, S>(a, s, tile_lane, h);
+    after();
+    return m;
+  }
+  float m = a.base;
+  const int nseq = seq_len<K>(a);
+  for (int c = 0; c < nseq; c += K) {
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+      m = walk_chunk<D, G, S>(s.cur, (int)(chunk_bytes_of(a, RB, c + j) / RB), tile_lane, h, m);
+      if (j == 0 && c == 0) after();
+      switch (j) {  // compile-time set index
+        case 0: stage_advance_regs<0, K, R>(a, RB, c + j, nseq, s); break;
+        case 1: stage_advance_regs<1, K, R>(a, RB, c + j, nseq, s); break;
+        case 2: if constexpr (K > 2) stage_advance_regs<2, K, R>(a, RB, c + j, nseq, s); break;
+        default: if constexpr (K > 3) stage_advance_regs<3, K, R>(a, RB, c + j, nseq, s); break;
+      }
+    }
+  }
+  return m;
+}
+
 // The round loop of a walk kernel, by regime.  kAny decides row prefetch and
 // staging at run time.  With S = 2 the kernels run a separate loop for
 // prefetched rows with a streamed ensemble and one with a resident ensemble
@@ -1023,8 +1053,11 @@ validity_kernel(WalkArgs a) {
   stage_prime(a, RB, st);
   auto rounds = [&](auto mode) {
     constexpr int M = decltype(mode)::value;
+    // streamed ensembles (register staging): a second batch, loaded after
+    // the first chunk
     constexpr int E = M >= kResident ? row_extra_batches<S, kValiditySets, Geo<S>::kStageRegs>()
-                                     : 0;
+                      : (M == kStreamed && S == 2) ? 1
+                                                   : 0;
     // lines shared by four lanes in the streamed kernel only (validity
     // 8.56 -> 8.31 ms on the 16M pool; the resident kernel of the HBM-bound
     // diagnostic ran 8 % slower with them)
@@ -1035,9 +1068,10 @@ validity_kernel(WalkArgs a) {
       const int64_t row = (tg * W + wave) * CPW + cl;
       const bool active = row < a.n;
       const int64_t rn = ((tg + gridDim.x) * W + wave) * CPW + cl;
+      constexpr bool split_loads = M == kResident || (M == kStreamed && E >= 1);
       if (pfr) {
         pf.commit(a, row, h, tile_lane);
-        if constexpr (M == kResident)
+        if constexpr (split_loads)
           pf.template load_batch<0>(a, rn, h);
         else
           pf.load(a, rn, h);
@@ -1050,6 +1084,10 @@ validity_kernel(WalkArgs a) {
         m = walk_chunk_after<D, G, S>(st.cur, a.ntrees, tile_lane, h, a.base,
                                       [&](int g) { pf.load_after_group(a, rn, h, g); });
         pf.load_rest(a, rn, h, walk_groups<D, G, S>(a.ntrees));
+      } else if constexpr (M == kStreamed && E >= 1) {
+        // kStreamed runs with register staging and more than one chunk
+        m = walk_all_after<D, G, S>(a, st, tile_lane, h,
+                                    [&]() { pf.template load_batch<1>(a, rn, h); });
       } else if constexpr (M == kResidentInline) {
         m = walk_chunk<D, G, S>(st.cur, a.ntrees, tile_lane, h, a.base);
       } else {
