@@ -107,6 +107,21 @@ def test_ragged_shallow_trees(monkeypatch, split, group):
     check_pipeline(V, P, X, 30)
 
 
+@pytest.mark.parametrize("split", [1, 2])
+def test_ragged_widest_rows(monkeypatch, split):
+    """256 features: the node word's feature byte offset reaches 255 x 256
+    (one lane per candidate) and its half (two lanes per candidate)."""
+    monkeypatch.setenv("ML2_WALK_SPLIT", str(split))
+    n, F, K = 1500, 256, 128
+    V = gen.ragged_ensemble(67, 1, 20, 9, F, K, 0.5, base_score=0.1, max_nodes=200)
+    P = gen.ragged_ensemble(67, 2, 30, 12, F, K, 0.1, max_nodes=300)
+    feats = np.concatenate([V.feature[V.left >= 0], P.feature[P.left >= 0]])
+    assert feats.max() >= 250, "the trees should split on the last features"
+    X = gen.features(67, n, F, K, missing=0.1)
+    _note(f"ragged F=256 S={split}: largest split feature {int(feats.max())}")
+    check_pipeline(V, P, X, 25)
+
+
 def test_forced_ragged_layout_on_perfect_trees(monkeypatch):
     """Perfect trees packed into ragged slots give the same results."""
     monkeypatch.setenv("ML2_LAYOUT", "ragged")
