@@ -52,7 +52,7 @@ typedef enum {
 
 /* Library limits (checked at load / call time, ML2_ERR_UNSUPPORTED beyond). */
 #define ML2_MAX_DEPTH 32        /* longest root-to-leaf path, in splits */
-#define ML2_MAX_TREE_NODES 2041 /* nodes of one tree in the ragged layout */
+#define ML2_MAX_TREE_NODES 3062 /* nodes of one tree in the ragged layout */
 #define ML2_MAX_FEATURES 256    /* num_features of an ensemble */
 #define ML2_MAX_TOPK 16384      /* k of ml2_filter_topk; m and keep of ml2_rerank */
 

@@ -36,7 +36,7 @@ constexpr int kMaxPerfectDepth = 12;  // deeper ensembles use the ragged layout
 //   then 8-byte nodes, each tree breadth-first (siblings adjacent):
 //     split: word 0 bit 31 default-left, bits 30..16 signed offset in nodes
 //            from the node to its left child (the right child follows it;
-//            trees have at most 2041 nodes), bits 15..8 split feature,
+//            trees have at most 3062 nodes), bits 15..8 split feature,
 //            bits 7..0 zero (bits 15..0: the feature's byte offset in a
 //            256-byte-row tile); word 1 threshold bits
 //     leaf:  word 0 0x7FFF0000 (offset -1, feature 0), word 1 the leaf

@@ -730,7 +730,7 @@ constexpr int row_extra_batches() {
   return S == 2 ? (K * R) / kRowBatch : 0;  // one lane per candidate: no room
 }
 
-// Lines shared by four lanes (P, S = 2): lanes (h, r, q) with h = lane bit
+// Lines shared by four lanes (Q, S = 2): lanes (h, r, q) with h = lane bit
 // 5, r = lane bit 4 and q = lane bits 3..0 hold candidates q + 16r.  The four
 // lanes (h, r) of candidates q and q+16 load the four vectors 4j..4j+3 (one
 // 64-byte half) of a line, first of row q, then of row q+16 (lane (h, r)

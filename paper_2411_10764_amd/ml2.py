@@ -22,7 +22,7 @@ ML2_ERR_UNSUPPORTED = 2
 ML2_ERR_OUT_OF_MEMORY = 3
 ML2_ERR_HIP = 4
 ML2_MAX_DEPTH = 32
-ML2_MAX_TREE_NODES = 2041
+ML2_MAX_TREE_NODES = 3062
 ML2_MAX_FEATURES = 256
 ML2_MAX_TOPK = 16384
 
