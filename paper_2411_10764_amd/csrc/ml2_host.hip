@@ -187,7 +187,10 @@ void pack_ragged(const std::vector<TreeView> &views, const std::vector<int> &dep
                  RaggedPack *out) {
   constexpr uint32_t CAP = ml2::kRaggedChunkBytes;
   constexpr int GRP = ml2::kRaggedGroup;
-  const uint32_t leaf_word0 = 0x7FFFu << 16;  // offset -1: the node itself
+  // a leaf's first word: offset -1 (the node itself) and, in the low half,
+  // the byte offset in the slot of the next tree's root (the sentinel after
+  // the last tree)
+  auto leaf_word0 = [](uint32_t next_root) { return (0x7FFFu << 16) | (8u * next_root); };
   auto bits = [](float v) {
     uint32_t b;
     memcpy(&b, &v, 4);
@@ -224,7 +227,7 @@ void pack_ragged(const std::vector<TreeView> &views, const std::vector<int> &dep
     for (size_t i = 0; i < ntr; ++i) {
       root[i] = head / 8u + next;
       if (i >= real) {  // padding: one leaf of value -0.0
-        node[next] = make_uint2(leaf_word0, bits(-0.0f));
+        node[next] = make_uint2(leaf_word0(head / 8u + next + 1), bits(-0.0f));
         ++next;
         continue;
       }
@@ -246,7 +249,8 @@ void pack_ragged(const std::vector<TreeView> &views, const std::vector<int> &dep
         const int32_t o = order[k];
         const uint32_t j = next + (uint32_t)k;
         if (tv.left[o] == -1) {
-          node[j] = make_uint2(leaf_word0, bits(tv.val[o]));
+          node[j] = make_uint2(leaf_word0(head / 8u + next + (uint32_t)order.size()),
+                               bits(tv.val[o]));
         } else {
           const int32_t rel = newid[(size_t)tv.left[o]] - (int32_t)k;  // nodes, > 0
           const uint32_t dl = (tv.dl && tv.dl[o]) ? 1u : 0u;
@@ -262,10 +266,11 @@ void pack_ragged(const std::vector<TreeView> &views, const std::vector<int> &dep
     // the sentinel: a leaf of value -0.0 that the two entries after the last
     // root point to (a walk past its last tree moves onto it; adding -0.0
     // changes no float)
-    node[next] = make_uint2(leaf_word0, bits(-0.0f));
-    root[ntr] = root[ntr + 1] = head / 8u + next;
+    const uint32_t sentinel = head / 8u + next;
+    node[next] = make_uint2(leaf_word0(sentinel), bits(-0.0f));
+    root[ntr] = root[ntr + 1] = sentinel;
     ++next;
-    const uint32_t hdr[4] = {(uint32_t)ntr, (uint32_t)depth, 0u, (uint32_t)tree_index};
+    const uint32_t hdr[4] = {(uint32_t)ntr, (uint32_t)depth, sentinel, (uint32_t)tree_index};
     memcpy(slot, hdr, sizeof hdr);
     tree_index += (int32_t)ntr;
     if (depth > out->depth) out->depth = depth;

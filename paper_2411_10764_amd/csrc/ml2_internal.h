@@ -30,7 +30,8 @@ constexpr int kMaxPerfectDepth = 12;  // deeper ensembles use the ragged layout
 // missing values): the ensemble is cut into chunks of whole trees, each in a
 // fixed slot of kRaggedChunkBytes bytes:
 //   byte 0   uint4 {trees in the chunk (a multiple of kRaggedGroup), deepest
-//            path of those trees, 0, global index of the chunk's first tree}
+//            path of those trees, the sentinel's node index, global index of
+//            the chunk's first tree}
 //   byte 16  uint32 root node index of each tree (node u at byte 8u of the
 //            slot), then two entries that point to the sentinel
 //   then 8-byte nodes, each tree breadth-first (siblings adjacent):
@@ -39,9 +40,11 @@ constexpr int kMaxPerfectDepth = 12;  // deeper ensembles use the ragged layout
 //            trees have at most 3062 nodes), bits 15..8 split feature,
 //            bits 7..0 zero (bits 15..0: the feature's byte offset in a
 //            256-byte-row tile); word 1 threshold bits
-//     leaf:  word 0 0x7FFF0000 (offset -1, feature 0), word 1 the leaf
-//            value; a walk treats a leaf as "go right", i.e. onto itself, so
-//            a lockstep walk may run past it
+//     leaf:  word 0 bits 31..16 0x7FFF (offset -1), bits 15..0 the byte
+//            offset in the slot of the next tree's root node (the
+//            sentinel's after the last tree; the sentinel's own); word 1 the
+//            leaf value.  A walk treats a leaf as "go right", i.e. onto
+//            itself, so a lockstep walk may run past it
 // Trees padded onto a chunk are single leaves of value -0.0; the sentinel,
 // after the last tree, is one more such leaf.
 constexpr uint32_t kRaggedChunkBytes = 24 * 1024;

@@ -338,7 +338,7 @@ struct RWalks {
     for (int g = 0; g < H; ++g) {
       const float t = __uint_as_float(nd[g].y);
       const bool missing_left = (int32_t)nd[g].x < 0 && __builtin_isnan(x[g]);
-      const bool right = nd[g].x == kLeafWord || (!(x[g] < t) && !missing_left);
+      const bool right = is_leaf(nd[g].x) || (!(x[g] < t) && !missing_left);
       const int32_t off = (int32_t)(nd[g].x << 1) >> 17;  // bits 30..16, signed
       u[g] = u[g] + (uint32_t)off + (right ? 1u : 0u);
     }
@@ -348,11 +348,11 @@ struct RWalks {
 #pragma unroll
     for (int g = 0; g < H; ++g) leaf[g] = __uint_as_float(nd[g].y);
   }
-  // Every walk of this lane is on a leaf (whose first word is kLeafWord).
+  // Every walk of this lane is on a leaf.
   __device__ __forceinline__ bool at_leaves() const {
     bool all = true;
 #pragma unroll
-    for (int g = 0; g < H; ++g) all = all && nd[g].x == kLeafWord;
+    for (int g = 0; g < H; ++g) all = all && is_leaf(nd[g].x);
     return all;
   }
   __device__ __forceinline__ float fold(float m) const {
@@ -365,19 +365,22 @@ struct RWalks {
     for (int g = 0; g < H; ++g) m = m + from_upper_half(leaf[g]);
     return m;
   }
-  static constexpr uint32_t kLeafWord = 0x7FFFu << 16;  // offset -1, feature 0
+  // a leaf's first word: offset -1 in bits 31..16 (no split has it)
+  __device__ __forceinline__ static bool is_leaf(uint32_t w0) { return (w0 >> 16) == 0x7FFFu; }
 };
 
 // Ragged chunk slot header (see ml2_internal.h), read from LDS into scalars.
 struct SlotHead {
   int ntrees;
   int depth;
+  uint32_t sentinel;  // node index of the slot's sentinel leaf
   int tree0;
 };
 
 __device__ __forceinline__ SlotHead slot_head(const char *slot) {
   const uint4 h = *reinterpret_cast<const uint4 *>(slot);
   return {__builtin_amdgcn_readfirstlane((int)h.x), __builtin_amdgcn_readfirstlane((int)h.y),
+          (uint32_t)__builtin_amdgcn_readfirstlane((int)h.z),
           __builtin_amdgcn_readfirstlane((int)h.w)};
 }
 
@@ -531,28 +534,21 @@ __device__ __forceinline__ float walk_slot_lanes(const char *slot, int ntr, int 
 
 // A ragged slot with one lane per candidate and one tree per lane: a walk on
 // a leaf adds the leaf's value and, in the same step, moves on to the root
-// of the lane's next tree, so no lane waits for another's path.  Past its
-// last tree a lane moves onto the slot's sentinel (two root entries after
-// the last tree, a leaf of value -0.0), and adding -0.0 leaves every float
-// unchanged, so a finished lane needs no test of its own.  The roots entry
-// of the next tree is read at every step.  The loop runs eight steps per
-// trip (one exit test per trip; a finished lane's extra steps change
-// nothing).  Every lane is done after at most (trees) x (depth + 1) steps;
+// of the lane's next tree, whose place the leaf holds, so no lane waits for
+// another's path.  The last tree's leaves lead to the slot's sentinel (a
+// leaf of value -0.0 that leads to itself), and adding -0.0 leaves every
+// float unchanged, so a finished lane needs no test of its own.  The loop
+// runs eight steps per trip (one exit test per trip: every lane on the
+// sentinel).  Every lane is done after at most (trees) x (depth + 1) steps;
 // the loop stops a little past that at the latest.
-__device__ __forceinline__ float walk_slot_single(const char *slot, int ntr, int depth,
+__device__ __forceinline__ float walk_slot_single(const char *slot, const SlotHead &hd,
                                                   const char *tile_lane, float m) {
   const uint32_t *roots = reinterpret_cast<const uint32_t *>(slot + 16);
   RWalks<1, 1> A;
   A.u[0] = roots[0];
   A.read_nodes(slot);
-  int t = 1;  // the roots entry of the lane's next tree (ntr + 1: done)
-  // read after the node, as the loop does (not folded into the read above),
-  // so that the loop starts with the reads in flight that it ends with
-  int t0 = 1;
-  asm volatile("" : "+v"(t0));
-  uint32_t nxt = roots[t0];
   __builtin_amdgcn_sched_barrier(0);
-  const int cap = ntr * (depth + 2) + 4;
+  const int cap = hd.ntrees * (hd.depth + 2) + 8;
   int it = 0;
   bool go = true;
   while (go) {
@@ -561,21 +557,19 @@ __device__ __forceinline__ float walk_slot_single(const char *slot, int ntr, int
       A.read_features(tile_lane);
       __builtin_amdgcn_sched_barrier(0);
       const uint32_t w0 = A.nd[0].x;
-      const bool leaf = w0 == RWalks<1, 1>::kLeafWord;
+      const bool leaf = RWalks<1, 1>::is_leaf(w0);
       m = m + (leaf ? __uint_as_float(A.nd[0].y) : -0.0f);
       const bool missing_left = (int32_t)w0 < 0 && __builtin_isnan(A.x[0]);
       const bool right = !(A.x[0] < __uint_as_float(A.nd[0].y)) && !missing_left;
       const int32_t off = (int32_t)(w0 << 1) >> 17;  // bits 30..16, signed
       uint32_t un = A.u[0] + (uint32_t)off + (right ? 1u : 0u);
       asm volatile("" : "+v"(un));  // computed by every lane: no branch
-      A.u[0] = leaf ? nxt : un;
-      t = min(t + (leaf ? 1 : 0), ntr + 1);
+      A.u[0] = leaf ? (w0 & 0xFFFFu) >> 3 : un;  // a leaf: its next root
       A.read_nodes(slot);
-      nxt = roots[t];
       __builtin_amdgcn_sched_barrier(0);
     }
     it += 8;
-    go = !__all(t > ntr) && it < cap;
+    go = !__all(A.u[0] == hd.sentinel) && it < cap;
   }
   return m;
 }
@@ -654,7 +648,7 @@ __device__ __forceinline__ float walk_chunk_after(const char *cb, int ntr, const
       const char *slot = cb + (uint32_t)i * RB;
       const SlotHead hd = slot_head(slot);
       if constexpr (S == 1 && G == 1) {
-        m = walk_slot_single(slot, hd.ntrees, hd.depth, tile_lane, m);
+        m = walk_slot_single(slot, hd, tile_lane, m);
       } else if constexpr (S == 1) {
         m = walk_slot_lanes<G>(slot, hd.ntrees, hd.depth, tile_lane, m);
       } else {
@@ -693,7 +687,7 @@ __device__ __forceinline__ float walk_chunk(const char *cb, int ntr, const char 
       const char *slot = cb + (uint32_t)i * RB;
       const SlotHead hd = slot_head(slot);
       if constexpr (S == 1 && G == 1) {
-        m = walk_slot_single(slot, hd.ntrees, hd.depth, tile_lane, m);
+        m = walk_slot_single(slot, hd, tile_lane, m);
       } else if constexpr (S == 1) {
         m = walk_slot_lanes<G>(slot, hd.ntrees, hd.depth, tile_lane, m);
       } else {
