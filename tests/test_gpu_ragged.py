@@ -122,6 +122,33 @@ def test_ragged_widest_rows(monkeypatch, split):
     check_pipeline(V, P, X, 25)
 
 
+@pytest.mark.parametrize("seed", range(12))
+def test_ragged_random_shapes(monkeypatch, seed):
+    """Seeded random ragged ensembles, feature counts, pool sizes (ragged
+    tails), missing fractions and launch shapes (lanes per candidate, trees
+    per lane), each against the oracle."""
+    rng = np.random.default_rng(1000 + seed)
+    F = int(rng.integers(1, 201))
+    K = int(rng.integers(0, F + 1))
+    n = int(rng.integers(1, 5000))
+    split = int(rng.choice([0, 1, 2]))
+    group = int(rng.choice([0, 1, 2, 4])) if split != 2 else int(rng.choice([0, 1, 2]))
+    for key, val in (("SPLIT", split), ("GROUP", group)):
+        if val:
+            monkeypatch.setenv(f"ML2_WALK_{key}", str(val))
+    V = gen.ragged_ensemble(2000 + seed, 1, int(rng.integers(1, 60)), int(rng.integers(1, 16)),
+                            F, K, 0.5, base_score=float(rng.normal(0, 0.5)),
+                            p_split=float(rng.uniform(0.5, 1.0)), max_nodes=int(rng.integers(3, 600)))
+    P = gen.ragged_ensemble(2000 + seed, 2, int(rng.integers(1, 120)), int(rng.integers(1, 16)),
+                            F, K, 0.1, p_split=float(rng.uniform(0.5, 1.0)),
+                            max_nodes=int(rng.integers(3, 600)))
+    X = gen.features(2000 + seed, n, F, K, missing=float(rng.choice([0.0, 0.05, 0.3])))
+    k = int(rng.integers(0, 200))
+    _note(f"random ragged seed={seed} F={F} K={K} n={n} S={split} G={group} "
+          f"V={V.num_trees} P={P.num_trees} k={k}")
+    check_pipeline(V, P, X, k)
+
+
 def test_forced_ragged_layout_on_perfect_trees(monkeypatch):
     """Perfect trees packed into ragged slots give the same results."""
     monkeypatch.setenv("ML2_LAYOUT", "ragged")
