@@ -219,6 +219,34 @@ def test_walk_plans(monkeypatch, split, group, waves, nbuf, chunk, depth):
     check_pipeline(V, P, X, 64)
 
 
+@pytest.mark.parametrize("seed", range(12))
+def test_perfect_random_shapes(monkeypatch, seed):
+    """Seeded random perfect ensembles (depth 1..12), feature counts, row
+    strides and alignment, pool sizes and launch plans (overrides that do not
+    fit are ignored by the planner), each against the oracle."""
+    rng = np.random.default_rng(3000 + seed)
+    depth = int(rng.integers(1, 13))
+    F = int(rng.integers(1, 257))
+    K = int(rng.integers(0, F + 1))
+    n = int(rng.integers(1, 4000))
+    ld = F + int(rng.choice([0, 0, 1, 3, 4]))
+    offset = int(rng.choice([0, 0, 1]))
+    for key, choices in (("SPLIT", [0, 1, 2]), ("GROUP", [0, 1, 2, 4, 8]), ("WAVES", [0, 4, 8]),
+                         ("NBUF", [0, 1, 2]), ("CHUNK", [0, 0, 16, 32])):
+        val = int(rng.choice(choices))
+        if val:
+            monkeypatch.setenv(f"ML2_WALK_{key}", str(val))
+    tv = int(rng.integers(1, 80)) if depth <= 9 else int(rng.integers(1, 12))
+    tp = int(rng.integers(1, 80)) if depth <= 9 else int(rng.integers(1, 12))
+    V = gen.perfect_ensemble(4000 + seed, 1, tv, depth, F, K, 0.5, float(rng.normal(0, 0.3)))
+    P = gen.perfect_ensemble(4000 + seed, 2, tp, depth, F, K, 0.1)
+    X = gen.features(4000 + seed, n, F, K)
+    k = int(rng.integers(0, 300))
+    _note(f"random perfect seed={seed} depth={depth} F={F} ld={ld} offset={offset} n={n} "
+          f"V={tv} P={tp} k={k}")
+    check_pipeline(V, P, X, k, ld=ld, offset=offset)
+
+
 @pytest.mark.parametrize("F,ld,trees", [(40, 40, 30), (128, 128, 48), (128, 131, 20),
                                          (132, 132, 16), (6, 6, 1)])
 def test_resident_ensemble(monkeypatch, F, ld, trees):
