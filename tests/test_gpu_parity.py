@@ -374,7 +374,7 @@ def test_repeatable_across_streams():
 # ---- full-size workloads: sampled outputs + properties -----------------------------
 
 @pytest.mark.slow
-@pytest.mark.parametrize("name", ["large", "roofline", "skewed", "hbm"])
+@pytest.mark.parametrize("name", ["large", "roofline", "skewed", "hbm", "paper"])
 def test_full_size_sampled(name):
     w = gen.WORKLOADS[name]
     _note(f"{name}: generating {w.n} x {w.F} features on the host")
