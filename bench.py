@@ -15,6 +15,7 @@ bounded sample of the same pool.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME]
     python bench.py --copy-probe      # plain 1 GiB device copies (counter scale)
+    python bench.py --probe           # LDS, VALU and walk-loop microbenchmarks
 """
 from __future__ import annotations
 
@@ -38,9 +39,9 @@ HBM_PEAK_GBS = 8000.0
 # (the 8-byte node and the 4-byte feature value).
 #   VALU: the fp32 vector peak of 157.3 TFLOP/s is 78.6 T lane-FMAs/s, i.e.
 #         128 lanes per clock per CU -> 39.3 T visits/s.
-#   LDS:  256 bytes per clock per CU (CDNA4 doubled CDNA3's 128; a streaming
-#         ds_read_b128 probe reaches 203 B/clk) -> 157 TB/s / 12 B = 13.1 T
-#         visits/s.
+#   LDS:  256 bytes per clock per CU (CDNA4 doubled CDNA3's 128; the
+#         consecutive 16-byte read probe of --probe reaches 160 B/clk)
+#         -> 157 TB/s / 12 B = 13.1 T visits/s.
 # The lower one, the LDS ceiling, is the peak.
 VALU_LANE_OPS_PER_S = 256 * 128 * 2.4e9
 VISIT_PEAK_VALU = VALU_LANE_OPS_PER_S / 2
@@ -83,6 +84,41 @@ def copy_probe() -> None:
         b.copy_(a)
     torch.cuda.synchronize()
     print(json.dumps({"copy_probe_bytes": 4 * n, "launches": 5}))
+
+
+def probes() -> None:
+    """Microbenchmarks of the units the walks use (include/ml2_probe.h), as
+    one JSON line: LDS bytes per clock per CU by read width and pattern,
+    32-bit add lane operations per second, and the walk's inner loop (a
+    resident chunk, no row loads or restaging) in node visits per second at
+    the 16M pool's two walk shapes.  Clock rates assume 2.4 GHz."""
+    import torch
+    from paper_2411_10764_amd import ml2
+    torch.cuda.init()
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    clk = 2.4e9
+    lds = {}
+    names = ["b32_consecutive", "b64_consecutive", "b128_consecutive",
+             "b32_random", "b64_random", "b128_random"]
+    for mode, name in enumerate(names):
+        ms, nbytes = ml2.ml2_probe_lds(mode, 2048, 4 * cus)
+        lds[name] = round(nbytes / (ms * 1e-3) / clk / cus, 1)
+    ms, ops = ml2.ml2_probe_valu(4096, 8 * cus)
+    valu = ops / (ms * 1e-3)
+    visit = {}
+    for depth in (6, 8):
+        ms, visits = ml2.ml2_probe_visit(depth, 512 if depth == 8 else 1024, 4 * cus)
+        visit[f"depth{depth}"] = {"tvisits_per_s": round(visits / (ms * 1e-3) / 1e12, 3),
+                                  "ms": round(ms, 3)}
+    print(json.dumps({
+        "probe": "ml2_probe_*", "cus": cus, "clock_ghz_assumed": clk / 1e9,
+        "lds_bytes_per_clk_per_cu": lds,
+        "lds_peak_bytes_per_clk_per_cu": LDS_BYTES_PER_S / clk / 256,
+        "valu_tlane_ops_per_s": round(valu / 1e12, 2),
+        "valu_peak_tlane_ops_per_s": round(VALU_LANE_OPS_PER_S / 1e12, 2),
+        "walk_loop": visit,
+        "visit_peak_tvisits_per_s": round(VISIT_PEAK_PER_S / 1e12, 2),
+    }), flush=True)
 
 
 def mean_path(ens, X) -> float:
@@ -215,6 +251,8 @@ def main() -> int:
     ap.add_argument("--cpu-rows", type=int, default=1 << 20)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-probe", action="store_true")
+    ap.add_argument("--probe", action="store_true",
+                    help="LDS / VALU / walk-loop microbenchmarks instead of the step")
     ap.add_argument("--explore", type=int, default=0, metavar="ROUNDS",
                     help="time ROUNDS explorer rounds (N = --N proposed per round, "
                          "(alpha+1)N held) instead of the scoring step")
@@ -224,6 +262,9 @@ def main() -> int:
 
     if args.copy_probe:
         copy_probe()
+        return 0
+    if args.probe:
+        probes()
         return 0
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "

@@ -15,6 +15,7 @@
 #include <vector>
 
 #include "ml2_internal.h"
+#include "ml2_probe.h"
 
 struct ml2_ensemble {
   ml2::Forest f;
@@ -301,6 +302,47 @@ ml2_status check_stream_args(const ml2_ensemble *e, const float *X, int64_t n, i
   if (*dev != e->f.device)
     return fail(ML2_ERR_INVALID_ARG, "%s: ensemble lives on device %d, current device is %d",
                 what, e->f.device, *dev);
+  return ML2_OK;
+}
+
+}  // namespace
+
+// Microbenchmark timing (ml2_probe.h).
+namespace {
+
+// One untimed and one timed launch of `launch` (which writes to a buffer of
+// out_bytes device bytes) on the null stream; *ms: the timed launch.
+template <typename Launch>
+ml2_status time_probe(const char *what, size_t out_bytes, double *ms, double *work,
+                      Launch launch) {
+  void *out = nullptr;
+  hipError_t e = hipMalloc(&out, out_bytes);
+  if (e != hipSuccess) return fail(ML2_ERR_OUT_OF_MEMORY, "%s: hipMalloc(%zu)", what, out_bytes);
+  hipEvent_t t0 = nullptr, t1 = nullptr;
+  float elapsed = 0.0f;
+  e = hipEventCreate(&t0);
+  if (e == hipSuccess) e = hipEventCreate(&t1);
+  if (e == hipSuccess) e = launch(out, work, nullptr);
+  if (e == hipSuccess) e = hipEventRecord(t0, nullptr);
+  if (e == hipSuccess) e = launch(out, work, nullptr);
+  if (e == hipSuccess) e = hipEventRecord(t1, nullptr);
+  if (e == hipSuccess) e = hipEventSynchronize(t1);
+  if (e == hipSuccess) e = hipEventElapsedTime(&elapsed, t0, t1);
+  if (t0) (void)hipEventDestroy(t0);
+  if (t1) (void)hipEventDestroy(t1);
+  (void)hipFree(out);
+  if (e != hipSuccess) return hip_fail(e, what);
+  *ms = elapsed;
+  return ML2_OK;
+}
+
+ml2_status check_probe(const char *what, int32_t iters, int32_t blocks, const double *ms,
+                       const double *work) {
+  if (!ms || !work) return fail(ML2_ERR_INVALID_ARG, "%s: NULL output", what);
+  if (iters < 1 || iters > (1 << 20))
+    return fail(ML2_ERR_INVALID_ARG, "%s: iters = %d outside [1, 2^20]", what, iters);
+  if (blocks < 1 || blocks > 65536)
+    return fail(ML2_ERR_INVALID_ARG, "%s: blocks = %d outside [1, 65536]", what, blocks);
   return ML2_OK;
 }
 
@@ -713,6 +755,43 @@ ml2_status ml2_explorer_round(ml2_explorer *ex, const float *X, int64_t ld, int3
   ex->rounds += 1;
   ex->scored = true;
   return ML2_OK;
+}
+
+// ---- microbenchmarks (ml2_probe.h) -------------------------------------------
+
+ml2_status ml2_probe_visit(int32_t depth, int32_t iters, int32_t blocks, double *ms,
+                           double *visits) {
+  ml2_status st = check_probe("ml2_probe_visit", iters, blocks, ms, visits);
+  if (st != ML2_OK) return st;
+  if (depth != 6 && depth != 8)
+    return fail(ML2_ERR_INVALID_ARG, "ml2_probe_visit: depth = %d (6 or 8)", depth);
+  return time_probe("ml2_probe_visit", (size_t)blocks * 256 * sizeof(float), ms, visits,
+                    [&](void *out, double *w, hipStream_t s) {
+                      return ml2::launch_visit_probe(depth, iters, blocks,
+                                                     static_cast<float *>(out), w, s);
+                    });
+}
+
+ml2_status ml2_probe_lds(int32_t mode, int32_t iters, int32_t blocks, double *ms, double *bytes) {
+  ml2_status st = check_probe("ml2_probe_lds", iters, blocks, ms, bytes);
+  if (st != ML2_OK) return st;
+  if (mode < 0 || mode > 5)
+    return fail(ML2_ERR_INVALID_ARG, "ml2_probe_lds: mode = %d outside [0, 5]", mode);
+  return time_probe("ml2_probe_lds", (size_t)blocks * 256 * sizeof(uint32_t), ms, bytes,
+                    [&](void *out, double *w, hipStream_t s) {
+                      return ml2::launch_lds_probe(mode, iters, blocks,
+                                                   static_cast<uint32_t *>(out), w, s);
+                    });
+}
+
+ml2_status ml2_probe_valu(int32_t iters, int32_t blocks, double *ms, double *lane_ops) {
+  ml2_status st = check_probe("ml2_probe_valu", iters, blocks, ms, lane_ops);
+  if (st != ML2_OK) return st;
+  return time_probe("ml2_probe_valu", (size_t)blocks * 256 * sizeof(uint32_t), ms, lane_ops,
+                    [&](void *out, double *w, hipStream_t s) {
+                      return ml2::launch_valu_probe(iters, blocks, static_cast<uint32_t *>(out),
+                                                    w, s);
+                    });
 }
 
 }  // extern "C"

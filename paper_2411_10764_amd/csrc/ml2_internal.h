@@ -113,4 +113,17 @@ hipError_t launch_rerank_select(const int32_t *rows, const float *scores, int32_
                                 int32_t keep, int32_t *idx, float *score, int32_t *num,
                                 hipStream_t s);
 
+// Microbenchmarks (measurement helpers behind the roofline figures).
+// Visit probe: the walk of a resident chunk of random perfect trees of depth
+// 6 or 8 over random 128-feature tiles, iters times per lane; *visits: the
+// node visits the launch makes.
+hipError_t launch_visit_probe(int depth, int iters, int blocks, float *out, double *visits,
+                              hipStream_t s);
+// LDS read probe (mode: 0..2 consecutive 4-, 8-, 16-byte reads per lane,
+// 3..5 the same at random addresses) and a 32-bit integer add probe; *work:
+// the bytes read or the lane operations of the launch.
+hipError_t launch_lds_probe(int mode, int iters, int blocks, uint32_t *out, double *work,
+                            hipStream_t s);
+hipError_t launch_valu_probe(int iters, int blocks, uint32_t *out, double *work, hipStream_t s);
+
 }  // namespace ml2

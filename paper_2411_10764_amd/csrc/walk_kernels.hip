@@ -1282,6 +1282,58 @@ constexpr bool group_allowed(int d, int g, int s) {
                  : (g == 1 || g == 2);
 }
 
+// ---- visit probe -----------------------------------------------------------
+
+__device__ __forceinline__ uint32_t probe_hash(uint32_t x) {
+  x ^= x >> 16;
+  x *= 0x7feb352du;
+  x ^= x >> 15;
+  x *= 0x846ca68bu;
+  x ^= x >> 16;
+  return x;
+}
+__device__ __forceinline__ float probe_unit(uint32_t i) {  // in [0, 1)
+  return (float)(probe_hash(i) >> 8) * (1.0f / 16777216.0f);
+}
+
+// The walks' inner loop alone: each workgroup fills its LDS with W candidate
+// tiles of F pseudo-random features in [0, 1) and one chunk of G*S perfect
+// trees of depth D (random split features below F, thresholds in [0, 1),
+// random leaves), then walks that chunk `iters` times with walk_chunk: the
+// node and feature reads, the child steps and the fold, without row loads,
+// restaging or barriers.  Every address stays in the tiles and the chunk.
+template <int D, int G, int S>
+__global__ void __launch_bounds__(kLanes *kMaxWaves) __attribute__((amdgpu_waves_per_eu(S, S)))
+visit_probe_kernel(float *out, int iters, int F, int W) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  constexpr uint32_t RB = record_bytes(D);
+  constexpr uint32_t L = 1u << D;
+  constexpr int CPW = Geo<S>::kCand;
+  const int lane = threadIdx.x & (kLanes - 1);
+  const int wave = threadIdx.x / kLanes;
+  const int h = lane / CPW;
+  const int cl = lane % CPW;
+  const uint32_t nthreads = (uint32_t)W * kLanes;
+  const uint32_t tile_bytes = (uint32_t)F * Geo<S>::kRowBytes;
+  char *chunk = smem + (uint32_t)W * tile_bytes;
+  float *tiles = reinterpret_cast<float *>(smem);
+  for (uint32_t i = threadIdx.x; i < (uint32_t)W * tile_bytes / 4u; i += nthreads)
+    tiles[i] = probe_unit(i + 0x51ED27u * blockIdx.x);
+  for (uint32_t i = threadIdx.x; i < (uint32_t)(G * S) * L; i += nthreads) {
+    const uint32_t t = i / L, j = i % L;
+    char *rec = chunk + t * RB;
+    if (j >= 1)
+      reinterpret_cast<uint2 *>(rec)[j] =
+          make_uint2(probe_hash(i ^ 0xA5A5A5u) % (uint32_t)F, __float_as_uint(probe_unit(i * 3u)));
+    reinterpret_cast<float *>(rec + 4u * L)[L + j] = probe_unit(i * 5u + 1u) - 0.5f;
+  }
+  __syncthreads();
+  const char *tile_lane = smem + (uint32_t)wave * tile_bytes + 4u * (uint32_t)cl;
+  float m = 0.0f;
+  for (int it = 0; it < iters; ++it) m = walk_chunk<D, G, S>(chunk, G * S, tile_lane, h, m);
+  if (h == 0) out[((size_t)blockIdx.x * W + wave) * CPW + cl] = m;
+}
+
 template <int D, int G, int S, bool RES>
 hipError_t launch_kernel(bool perf, const WalkPlan &p, const WalkArgs &a, hipStream_t s) {
   const void *fn = perf ? reinterpret_cast<const void *>(&perf_kernel<D, G, S, RES>)
@@ -1591,6 +1643,37 @@ hipError_t launch_rows(const Forest &f, const float *X, int64_t n, int64_t ld, c
   hipError_t e = launch_leaves(D, a, G, W, lds, row_tiles, s);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(fold_kernel, dim3((unsigned)((m + 255) / 256)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+// The visit probe at the 16M pool's walk shapes: depth 6 with eight trees
+// per lane or depth 8 with four, two lanes per candidate, eight waves, 128
+// features.  out: blocks * 256 floats.
+hipError_t launch_visit_probe(int depth, int iters, int blocks, float *out, double *visits,
+                              hipStream_t s) {
+  constexpr int S = 2, W = 8, F = 128;
+  const void *fn = nullptr;
+  int G = 0;
+  if (depth == 6) {
+    fn = reinterpret_cast<const void *>(&visit_probe_kernel<6, 8, S>);
+    G = 8;
+  } else if (depth == 8) {
+    fn = reinterpret_cast<const void *>(&visit_probe_kernel<8, 4, S>);
+    G = 4;
+  } else {
+    return hipErrorInvalidValue;
+  }
+  const size_t lds = (size_t)W * F * Geo<S>::kRowBytes + (size_t)G * S * record_bytes(depth);
+  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  if (depth == 6)
+    hipLaunchKernelGGL((visit_probe_kernel<6, 8, S>), dim3(blocks), dim3(W * kLanes), lds, s, out,
+                       iters, F, W);
+  else
+    hipLaunchKernelGGL((visit_probe_kernel<8, 4, S>), dim3(blocks), dim3(W * kLanes), lds, s, out,
+                       iters, F, W);
+  // candidates x trees x levels
+  *visits = (double)blocks * W * Geo<S>::kCand * (double)iters * G * S * depth;
   return hipGetLastError();
 }
 

@@ -34,6 +34,8 @@ EXPORTED = (
     "ml2_explorer_create", "ml2_explorer_free", "ml2_explorer_reset", "ml2_explorer_rounds",
     "ml2_explorer_round", "ml2_last_error",
 )
+# include/ml2_probe.h: microbenchmarks behind the roofline figures
+EXPORTED_PROBE = ("ml2_probe_visit", "ml2_probe_lds", "ml2_probe_valu")
 
 
 class Ml2Error(RuntimeError):
@@ -100,6 +102,13 @@ def lib():
         L.ml2_explorer_round.argtypes = [P, P, I64, I32, P, P, P, P]
         L.ml2_last_error.restype = ctypes.c_char_p
         L.ml2_last_error.argtypes = []
+        D = ctypes.POINTER(ctypes.c_double)
+        L.ml2_probe_visit.restype = I32
+        L.ml2_probe_visit.argtypes = [I32, I32, I32, D, D]
+        L.ml2_probe_lds.restype = I32
+        L.ml2_probe_lds.argtypes = [I32, I32, I32, D, D]
+        L.ml2_probe_valu.restype = I32
+        L.ml2_probe_valu.argtypes = [I32, I32, D, D]
         _lib = L
     return _lib
 
@@ -316,3 +325,27 @@ class Pipeline:
         ml2_score_perf(self.p, X, self.valid, self.score, stream)
         ml2_filter_topk(self.valid, self.score, self.k, self.idx, self.top, self.num, self.ws,
                         self.ws_bytes, self.n, stream)
+
+
+# ---- microbenchmarks (include/ml2_probe.h) ---------------------------------
+
+def _probe(fn, *args):
+    ms, work = ctypes.c_double(), ctypes.c_double()
+    _check(fn(*args, ctypes.byref(ms), ctypes.byref(work)))
+    return ms.value, work.value
+
+
+def ml2_probe_visit(depth: int, iters: int, blocks: int):
+    """(ms, node visits) of the walk's inner loop over a resident chunk."""
+    return _probe(lib().ml2_probe_visit, depth, iters, blocks)
+
+
+def ml2_probe_lds(mode: int, iters: int, blocks: int):
+    """(ms, bytes read) of LDS reads of 4/8/16 bytes (mode % 3), consecutive
+    (mode < 3) or random."""
+    return _probe(lib().ml2_probe_lds, mode, iters, blocks)
+
+
+def ml2_probe_valu(iters: int, blocks: int):
+    """(ms, lane additions) of chains of 32-bit adds."""
+    return _probe(lib().ml2_probe_valu, iters, blocks)

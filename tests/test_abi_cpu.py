@@ -13,10 +13,11 @@ from paper_2411_10764_amd import ml2
 from tests.treeutil import ensemble_from_trees
 
 HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "ml2.h")
+PROBE_HEADER = os.path.join(os.path.dirname(HEADER), "ml2_probe.h")
 
 
-def _header_functions():
-    text = open(HEADER).read()
+def _header_functions(path=HEADER):
+    text = open(path).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(ml2_[a-z_]+)\s*\(", text)))
 
@@ -28,6 +29,32 @@ def test_exports_every_declared_symbol():
     for name in declared:
         assert hasattr(L, name), f"{name} not exported"
     assert sorted(ml2.EXPORTED) == declared
+
+
+def test_exports_every_probe_symbol():
+    L = ml2.lib()
+    declared = _header_functions(PROBE_HEADER)
+    assert declared == sorted(ml2.EXPORTED_PROBE)
+    for name in declared:
+        assert hasattr(L, name), f"{name} not exported"
+
+
+@pytest.mark.parametrize("call", [
+    lambda L, ms, w: L.ml2_probe_visit(7, 10, 4, ms, w),      # depth 6 or 8 only
+    lambda L, ms, w: L.ml2_probe_visit(8, 0, 4, ms, w),       # iters >= 1
+    lambda L, ms, w: L.ml2_probe_visit(8, 10, 0, ms, w),      # blocks >= 1
+    lambda L, ms, w: L.ml2_probe_visit(8, 10, 4, None, w),    # NULL output
+    lambda L, ms, w: L.ml2_probe_lds(6, 10, 4, ms, w),        # mode 0..5
+    lambda L, ms, w: L.ml2_probe_lds(0, 1 << 21, 4, ms, w),   # iters <= 2^20
+    lambda L, ms, w: L.ml2_probe_lds(0, 10, 65537, ms, w),    # blocks <= 65536
+    lambda L, ms, w: L.ml2_probe_valu(10, 4, ms, None),       # NULL output
+])
+def test_probe_argument_errors(call):
+    """Probe arguments are checked before any HIP call."""
+    L = ml2.lib()
+    ms, w = ctypes.c_double(-1.0), ctypes.c_double(-1.0)
+    assert call(L, ctypes.byref(ms), ctypes.byref(w)) == ml2.ML2_ERR_INVALID_ARG
+    assert ms.value == -1.0 and w.value == -1.0
 
 
 def test_header_constants_match_binding():
