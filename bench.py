@@ -106,17 +106,21 @@ def probes() -> None:
     ms, ops = ml2.ml2_probe_valu(4096, 8 * cus)
     valu = ops / (ms * 1e-3)
     visit = {}
-    for depth in (6, 8):
-        ms, visits = ml2.ml2_probe_visit(depth, 512 if depth == 8 else 1024, 4 * cus)
-        visit[f"depth{depth}"] = {"tvisits_per_s": round(visits / (ms * 1e-3) / 1e12, 3),
-                                  "ms": round(ms, 3)}
+    # (depth, trees per lane, lanes per candidate, waves, features): the 16M
+    # pool's validity and perf walks first, then other shapes of depth 8
+    shapes = [(6, 8, 2, 8, 128), (8, 4, 2, 8, 128), (8, 2, 2, 8, 128), (8, 4, 2, 4, 128),
+              (8, 8, 2, 4, 128), (8, 4, 2, 8, 64), (8, 8, 2, 8, 64), (8, 4, 1, 8, 64),
+              (8, 8, 1, 8, 64)]
+    for d, g, s_, w, f in shapes:
+        ms, visits = ml2.ml2_probe_visit(d, g, s_, w, f, 512 if d == 8 else 1024, 4 * cus)
+        visit[f"D{d}_G{g}_S{s_}_W{w}_F{f}"] = round(visits / (ms * 1e-3) / 1e12, 3)
     print(json.dumps({
         "probe": "ml2_probe_*", "cus": cus, "clock_ghz_assumed": clk / 1e9,
         "lds_bytes_per_clk_per_cu": lds,
         "lds_peak_bytes_per_clk_per_cu": LDS_BYTES_PER_S / clk / 256,
         "valu_tlane_ops_per_s": round(valu / 1e12, 2),
         "valu_peak_tlane_ops_per_s": round(VALU_LANE_OPS_PER_S / 1e12, 2),
-        "walk_loop": visit,
+        "walk_loop_tvisits_per_s": visit,
         "visit_peak_tvisits_per_s": round(VISIT_PEAK_PER_S / 1e12, 2),
     }), flush=True)
 

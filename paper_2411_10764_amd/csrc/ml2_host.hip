@@ -759,15 +759,27 @@ ml2_status ml2_explorer_round(ml2_explorer *ex, const float *X, int64_t ld, int3
 
 // ---- microbenchmarks (ml2_probe.h) -------------------------------------------
 
-ml2_status ml2_probe_visit(int32_t depth, int32_t iters, int32_t blocks, double *ms,
-                           double *visits) {
+ml2_status ml2_probe_visit(int32_t depth, int32_t trees_per_lane, int32_t lanes_per_candidate,
+                           int32_t waves, int32_t features, int32_t iters, int32_t blocks,
+                           double *ms, double *visits) {
   ml2_status st = check_probe("ml2_probe_visit", iters, blocks, ms, visits);
   if (st != ML2_OK) return st;
-  if (depth != 6 && depth != 8)
-    return fail(ML2_ERR_INVALID_ARG, "ml2_probe_visit: depth = %d (6 or 8)", depth);
-  return time_probe("ml2_probe_visit", (size_t)blocks * 256 * sizeof(float), ms, visits,
+  const int G = trees_per_lane, S = lanes_per_candidate;
+  const bool shape_ok = (depth == 6 || depth == 8) &&
+                        ((S == 2 && (G == 2 || G == 4 || G == 8)) || (S == 1 && (G == 4 || G == 8))) &&
+                        (waves == 4 || waves == 8) && (features == 64 || features == 128);
+  if (!shape_ok)
+    return fail(ML2_ERR_INVALID_ARG,
+                "ml2_probe_visit: shape depth %d, %d trees per lane, %d lanes per candidate, %d "
+                "waves, %d features not built",
+                depth, G, S, waves, features);
+  const size_t lds = (size_t)waves * features * 4 * (64 / S) + (size_t)G * S * ml2::record_bytes(depth);
+  if (lds > ml2::kLdsBudget)
+    return fail(ML2_ERR_INVALID_ARG, "ml2_probe_visit: %zu bytes of LDS needed (%zu available)",
+                lds, (size_t)ml2::kLdsBudget);
+  return time_probe("ml2_probe_visit", (size_t)blocks * 512 * sizeof(float), ms, visits,
                     [&](void *out, double *w, hipStream_t s) {
-                      return ml2::launch_visit_probe(depth, iters, blocks,
+                      return ml2::launch_visit_probe(depth, G, S, waves, features, iters, blocks,
                                                      static_cast<float *>(out), w, s);
                     });
 }

@@ -24,6 +24,7 @@ namespace ml2 {
 // taken otherwise, so a walk moves with u <- 2u + [x < t].  Byte 0..7 is
 // unused.
 constexpr int kTreePad = 16;  // >= the trees of the largest walk group
+constexpr size_t kLdsBudget = 160 * 1024 - 256;  // LDS of a walk workgroup (static LDS headroom)
 constexpr int kMaxPerfectDepth = 12;  // deeper ensembles use the ragged layout
 
 // Ragged layout (deep or sparse trees, or per-node default directions for
@@ -115,10 +116,12 @@ hipError_t launch_rerank_select(const int32_t *rows, const float *scores, int32_
 
 // Microbenchmarks (measurement helpers behind the roofline figures).
 // Visit probe: the walk of a resident chunk of random perfect trees of depth
-// 6 or 8 over random 128-feature tiles, iters times per lane; *visits: the
-// node visits the launch makes.
-hipError_t launch_visit_probe(int depth, int iters, int blocks, float *out, double *visits,
-                              hipStream_t s);
+// 6 or 8 over random feature tiles, iters times per lane, at the shape
+// (trees per lane G, lanes per candidate S, waves, features); *visits: the
+// node visits the launch makes.  hipErrorInvalidValue for a shape it does
+// not build or whose tiles and chunk exceed the LDS.
+hipError_t launch_visit_probe(int depth, int G, int S, int waves, int features, int iters,
+                              int blocks, float *out, double *visits, hipStream_t s);
 // LDS read probe (mode: 0..2 consecutive 4-, 8-, 16-byte reads per lane,
 // 3..5 the same at random addresses) and a 32-bit integer add probe; *work:
 // the bytes read or the lane operations of the launch.

@@ -46,7 +46,6 @@ namespace ml2 {
 namespace {
 
 constexpr int kLanes = 64;
-constexpr size_t kLdsBudget = 160 * 1024 - 256;  // headroom for static LDS
 constexpr int kMaxWaves = 8;
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -1646,35 +1645,50 @@ hipError_t launch_rows(const Forest &f, const float *X, int64_t n, int64_t ld, c
   return hipGetLastError();
 }
 
-// The visit probe at the 16M pool's walk shapes: depth 6 with eight trees
-// per lane or depth 8 with four, two lanes per candidate, eight waves, 128
-// features.  out: blocks * 256 floats.
-hipError_t launch_visit_probe(int depth, int iters, int blocks, float *out, double *visits,
-                              hipStream_t s) {
-  constexpr int S = 2, W = 8, F = 128;
-  const void *fn = nullptr;
-  int G = 0;
-  if (depth == 6) {
-    fn = reinterpret_cast<const void *>(&visit_probe_kernel<6, 8, S>);
-    G = 8;
-  } else if (depth == 8) {
-    fn = reinterpret_cast<const void *>(&visit_probe_kernel<8, 4, S>);
-    G = 4;
-  } else {
-    return hipErrorInvalidValue;
-  }
-  const size_t lds = (size_t)W * F * Geo<S>::kRowBytes + (size_t)G * S * record_bytes(depth);
+template <int D, int G, int S>
+hipError_t launch_visit_probe_dgs(int waves, int features, int iters, int blocks, float *out,
+                                  double *visits, hipStream_t s) {
+  const void *fn = reinterpret_cast<const void *>(&visit_probe_kernel<D, G, S>);
+  const size_t lds =
+      (size_t)waves * features * Geo<S>::kRowBytes + (size_t)G * S * record_bytes(D);
+  if (lds > kLdsBudget) return hipErrorInvalidValue;
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  if (depth == 6)
-    hipLaunchKernelGGL((visit_probe_kernel<6, 8, S>), dim3(blocks), dim3(W * kLanes), lds, s, out,
-                       iters, F, W);
-  else
-    hipLaunchKernelGGL((visit_probe_kernel<8, 4, S>), dim3(blocks), dim3(W * kLanes), lds, s, out,
-                       iters, F, W);
+  hipLaunchKernelGGL((visit_probe_kernel<D, G, S>), dim3(blocks), dim3(waves * kLanes), lds, s,
+                     out, iters, features, waves);
   // candidates x trees x levels
-  *visits = (double)blocks * W * Geo<S>::kCand * (double)iters * G * S * depth;
+  *visits = (double)blocks * waves * Geo<S>::kCand * (double)iters * G * S * D;
   return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_visit_probe_d(int G, int S, int waves, int features, int iters, int blocks,
+                                float *out, double *visits, hipStream_t s) {
+  if (S == 2 && G == 2)
+    return launch_visit_probe_dgs<D, 2, 2>(waves, features, iters, blocks, out, visits, s);
+  if (S == 2 && G == 4)
+    return launch_visit_probe_dgs<D, 4, 2>(waves, features, iters, blocks, out, visits, s);
+  if (S == 2 && G == 8)
+    return launch_visit_probe_dgs<D, 8, 2>(waves, features, iters, blocks, out, visits, s);
+  if (S == 1 && G == 4)
+    return launch_visit_probe_dgs<D, 4, 1>(waves, features, iters, blocks, out, visits, s);
+  if (S == 1 && G == 8)
+    return launch_visit_probe_dgs<D, 8, 1>(waves, features, iters, blocks, out, visits, s);
+  return hipErrorInvalidValue;
+}
+
+// The visit probe: depth 6 or 8; (G, S) one of (2, 2), (4, 2), (8, 2),
+// (4, 1), (8, 1); 4 or 8 waves; 64 or 128 features; the tiles and the chunk
+// must fit the LDS of one workgroup.  out: blocks * 512 floats.
+hipError_t launch_visit_probe(int depth, int G, int S, int waves, int features, int iters,
+                              int blocks, float *out, double *visits, hipStream_t s) {
+  if ((waves != 4 && waves != 8) || (features != 64 && features != 128))
+    return hipErrorInvalidValue;
+  if (depth == 6)
+    return launch_visit_probe_d<6>(G, S, waves, features, iters, blocks, out, visits, s);
+  if (depth == 8)
+    return launch_visit_probe_d<8>(G, S, waves, features, iters, blocks, out, visits, s);
+  return hipErrorInvalidValue;
 }
 
 }  // namespace ml2

@@ -104,7 +104,7 @@ def lib():
         L.ml2_last_error.argtypes = []
         D = ctypes.POINTER(ctypes.c_double)
         L.ml2_probe_visit.restype = I32
-        L.ml2_probe_visit.argtypes = [I32, I32, I32, D, D]
+        L.ml2_probe_visit.argtypes = [I32, I32, I32, I32, I32, I32, I32, D, D]
         L.ml2_probe_lds.restype = I32
         L.ml2_probe_lds.argtypes = [I32, I32, I32, D, D]
         L.ml2_probe_valu.restype = I32
@@ -335,9 +335,12 @@ def _probe(fn, *args):
     return ms.value, work.value
 
 
-def ml2_probe_visit(depth: int, iters: int, blocks: int):
-    """(ms, node visits) of the walk's inner loop over a resident chunk."""
-    return _probe(lib().ml2_probe_visit, depth, iters, blocks)
+def ml2_probe_visit(depth: int, trees_per_lane: int, lanes_per_candidate: int, waves: int,
+                    features: int, iters: int, blocks: int):
+    """(ms, node visits) of the walk's inner loop over a resident chunk at
+    the given shape."""
+    return _probe(lib().ml2_probe_visit, depth, trees_per_lane, lanes_per_candidate, waves,
+                  features, iters, blocks)
 
 
 def ml2_probe_lds(mode: int, iters: int, blocks: int):

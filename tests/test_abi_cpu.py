@@ -40,10 +40,13 @@ def test_exports_every_probe_symbol():
 
 
 @pytest.mark.parametrize("call", [
-    lambda L, ms, w: L.ml2_probe_visit(7, 10, 4, ms, w),      # depth 6 or 8 only
-    lambda L, ms, w: L.ml2_probe_visit(8, 0, 4, ms, w),       # iters >= 1
-    lambda L, ms, w: L.ml2_probe_visit(8, 10, 0, ms, w),      # blocks >= 1
-    lambda L, ms, w: L.ml2_probe_visit(8, 10, 4, None, w),    # NULL output
+    lambda L, ms, w: L.ml2_probe_visit(7, 4, 2, 8, 128, 10, 4, ms, w),    # depth 6 or 8
+    lambda L, ms, w: L.ml2_probe_visit(8, 2, 1, 8, 64, 10, 4, ms, w),     # shape not built
+    lambda L, ms, w: L.ml2_probe_visit(8, 8, 2, 8, 128, 10, 4, ms, w),    # beyond the LDS
+    lambda L, ms, w: L.ml2_probe_visit(8, 4, 2, 6, 128, 10, 4, ms, w),    # 4 or 8 waves
+    lambda L, ms, w: L.ml2_probe_visit(8, 4, 2, 8, 128, 0, 4, ms, w),     # iters >= 1
+    lambda L, ms, w: L.ml2_probe_visit(8, 4, 2, 8, 128, 10, 0, ms, w),    # blocks >= 1
+    lambda L, ms, w: L.ml2_probe_visit(8, 4, 2, 8, 128, 10, 4, None, w),  # NULL output
     lambda L, ms, w: L.ml2_probe_lds(6, 10, 4, ms, w),        # mode 0..5
     lambda L, ms, w: L.ml2_probe_lds(0, 1 << 21, 4, ms, w),   # iters <= 2^20
     lambda L, ms, w: L.ml2_probe_lds(0, 10, 65537, ms, w),    # blocks <= 65536

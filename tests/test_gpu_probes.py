@@ -9,11 +9,12 @@ torch = pytest.importorskip("torch")
 from paper_2411_10764_amd import ml2  # noqa: E402
 
 
-@pytest.mark.parametrize("depth", [6, 8])
-def test_visit_probe(depth):
-    ms, visits = ml2.ml2_probe_visit(depth, 4, 8)
-    G = 8 if depth == 6 else 4
-    assert visits == 8 * 8 * 32 * 4 * (2 * G) * depth
+@pytest.mark.parametrize("depth,G,S,waves,F", [
+    (6, 8, 2, 8, 128), (8, 4, 2, 8, 128), (8, 2, 2, 8, 128), (8, 8, 2, 8, 64), (8, 8, 2, 4, 128),
+    (8, 4, 1, 8, 64), (8, 8, 1, 8, 64), (6, 4, 2, 4, 64)])
+def test_visit_probe(depth, G, S, waves, F):
+    ms, visits = ml2.ml2_probe_visit(depth, G, S, waves, F, 4, 8)
+    assert visits == 8 * waves * (64 // S) * 4 * (G * S) * depth
     assert ms > 0.0
 
 
