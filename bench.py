@@ -271,7 +271,7 @@ def main() -> int:
         probes()
         return 0
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
+        print(f"bench.py: the scoring path runs on one GPU; --gpus {args.gpus} is not supported "
               "(the pool would shard by rows with one all-gather of the per-GPU top-k lists).",
               file=sys.stderr)
         return 2
