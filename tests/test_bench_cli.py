@@ -1,0 +1,59 @@
+"""Host logic of bench.py that runs without a GPU: the one-GPU contract, the
+visit ceiling it prices the walks against, and the staleness rule of the
+committed HBM-traffic counters."""
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+
+
+@pytest.mark.parametrize("gpus", [2, 8])
+def test_more_than_one_gpu_is_refused(gpus):
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", str(gpus)],
+                       capture_output=True, text=True, timeout=120, cwd=ROOT)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+    assert r.stdout.strip() == ""  # no JSON line for an unsupported run
+
+
+def test_visit_ceiling_from_unit_counts():
+    # 256 CUs at 2.4 GHz: LDS 256 B/clk/CU over 12 B per visit, VALU 128
+    # lanes/clk/CU over 2 instructions per visit; the lower one is the peak.
+    lds = 256 * 256 * 2.4e9 / 12
+    valu = 256 * 128 * 2.4e9 / 2
+    assert bench.VISIT_PEAK_LDS == pytest.approx(lds)
+    assert bench.VISIT_PEAK_VALU == pytest.approx(valu)
+    assert bench.VISIT_PEAK_PER_S == pytest.approx(min(lds, valu))
+    assert bench.VISIT_PEAK_PER_S == pytest.approx(13.1072e12)
+
+
+def test_traffic_only_for_the_profiled_source(tmp_path, monkeypatch):
+    sha = bench._kernel_sha()
+    f = tmp_path / "traffic.json"
+    f.write_text(json.dumps({"kernel_source_sha256": sha, "bytes_per_launch": 123.0}))
+    monkeypatch.setattr(bench, "TRAFFIC_FILE", str(f))
+    assert bench._traffic(sha) == 123.0
+    assert bench._traffic("0" * 64) is None  # counters taken on other source
+    monkeypatch.setattr(bench, "TRAFFIC_FILE", str(tmp_path / "missing.json"))
+    assert bench._traffic(sha) is None
+
+
+def test_committed_traffic_matches_current_source():
+    """The committed counters were taken on the walk kernels as they stand;
+    a kernel change makes bench.py report traffic as null until the
+    counters are taken again."""
+    with open(bench.TRAFFIC_FILE) as fh:
+        t = json.load(fh)
+    if t["kernel_source_sha256"] != bench._kernel_sha():
+        pytest.skip("walk kernels changed since the counters were taken (traffic reported null)")
+    copy = t["copy_probe"]
+    want = (t["fetch_size_kib"] * 1024 / copy["fetch_factor"]
+            + t["write_size_kib"] * 1024 / copy["write_factor"])
+    assert t["bytes_per_launch"] == pytest.approx(want, rel=1e-9)
