@@ -183,7 +183,8 @@ ml2_status ml2_filter_topk(const uint8_t *valid, const float *scores, int64_t n,
  * row ascending (-0.0 and +0.0 are equal; a row listed twice is taken twice).
  * Writes
  *   out_idx[j], out_score[j]  for j < min(keep, #in range): pool row and its
- *                             score (a zero score is written as +0.0)
+ *                             score (bit-exact copy of the entry's row_scores
+ *                             value, sign of zero included)
  *   out_idx[j] = -1, out_score[j] = -inf for the remaining slots
  *   *num_selected = min(keep, #in range)        (int32, device)
  * X: float32 [n][ld] device, as in ml2_score_validity (a's features may be

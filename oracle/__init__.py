@@ -204,8 +204,7 @@ def explore(v_ens, p_ens, a_ens, X, k: int, keep: int, rounds: int, threads: int
     each round holds the k best accepted rows not proposed before (by P),
     model A (or P's order when a_ens is None) keeps `keep` of them, and those
     are proposed.  Returns [(idx i32 [keep], score f32 [keep], num)] per
-    round; -1/-inf pad a round once the pool runs dry; a zero score is
-    reported as +0.0."""
+    round; -1/-inf pad a round once the pool runs dry."""
     valid, _ = validity(v_ens, X, threads)
     score = perf(p_ens, X, valid, threads)
     proposed = np.zeros(valid.shape[0], bool)
@@ -217,7 +216,6 @@ def explore(v_ens, p_ens, a_ens, X, k: int, keep: int, rounds: int, threads: int
             _, idx, top, num = rerank(a_ens, X, held, keep)
         else:
             idx, top = held[:keep].copy(), held_score[:keep].copy()
-            top[top == 0] = 0.0
             num = min(n_held, keep)
         proposed[idx[idx >= 0]] = True
         out.append((idx, top, num))

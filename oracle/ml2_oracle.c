@@ -221,10 +221,10 @@ int64_t ml2o_topk(const uint8_t *valid, const float *score, int64_t n, int64_t k
  * rows[0..m) list pool rows of X (n rows, stride ld).  Entry i with
  * 0 <= rows[i] < n gets row_scores[i] = margin under a; any other entry gets
  * -inf and is skipped.  The scored entries are ordered by (score desc, row
- * asc), a row listed twice counting twice, and the first min(keep, #scored)
- * are written (a zero score as +0.0, since -0 == +0 in the order); the other
- * keep slots get -1 / -inf.  Returns the number written, -1 on allocation
- * failure.
+ * asc; -0 == +0), a row listed twice counting twice, and the first
+ * min(keep, #scored) are written with the row and that entry's score as
+ * computed (sign of zero included); the other keep slots get -1 / -inf.
+ * Returns the number written, -1 on allocation failure.
  */
 int64_t ml2o_rerank(const ml2o_ensemble *a, const float *X, int64_t n, int64_t ld,
                     const int32_t *rows, int64_t m, int64_t keep, float *row_scores,
@@ -250,7 +250,7 @@ int64_t ml2o_rerank(const ml2o_ensemble *a, const float *X, int64_t n, int64_t l
   for (int64_t j = 0; j < keep; ++j) {
     if (j < sel) {
       idx[j] = (int32_t)all[j].i;
-      out_score[j] = (all[j].s == 0.0f) ? 0.0f : all[j].s;
+      out_score[j] = all[j].s;
     } else {
       idx[j] = -1;
       out_score[j] = -INFINITY;

@@ -236,10 +236,28 @@ __device__ __forceinline__ float key_score(unsigned long long key) {
   return __uint_as_float(b);
 }
 
+// Key of a listed row for the second-level selection: the high word orders
+// by score (-0.0 and +0.0 equal), the low word by pool row ascending
+// (0x7FFFFFFF - row, row < 2^31, in bits 31..1) and keeps, in bit 0, the
+// sign of a zero score, so that the chosen entry's score comes back bit for
+// bit.  Two entries of one row carry the same score (the same row walked by
+// the same model), so bit 0 never reorders distinct scores.
+__device__ __forceinline__ unsigned long long row_key(float s, int32_t row) {
+  const uint32_t neg_zero = (__float_as_uint(s) == 0x80000000u) ? 1u : 0u;
+  const uint32_t lo = ((0x7FFFFFFFu - (uint32_t)row) << 1) | neg_zero;
+  return (make_key(s, 0) & 0xFFFFFFFF00000000ull) | (unsigned long long)lo;
+}
+__device__ __forceinline__ int32_t row_key_row(unsigned long long key) {
+  return (int32_t)(0x7FFFFFFFu - ((uint32_t)key >> 1));
+}
+__device__ __forceinline__ float row_key_score(unsigned long long key) {
+  return (key & 1ull) ? -0.0f : key_score(key);
+}
+
 // Second-level selection (model A): one workgroup sorts the keys of the m
-// listed rows, (ord(score) << 32) | (0xFFFFFFFF - row), and writes the best
-// `keep`.  Rows outside [0, n) and NaN scores are left out (key 0, below
-// every included key: a zero high word is the ord of a negative NaN).
+// listed rows (row_key) and writes the best `keep`.  Rows outside [0, n)
+// and NaN scores are left out (key 0, below every included key: a zero high
+// word is the ord of a negative NaN).
 __global__ void __launch_bounds__(kSortThreads) rerank_select(const int32_t *rows,
                                                               const float *scores, int32_t m,
                                                               int64_t n, int32_t keep,
@@ -258,7 +276,7 @@ __global__ void __launch_bounds__(kSortThreads) rerank_select(const int32_t *row
       const int32_t r = rows[j];
       const float sc = scores[j];
       if (r >= 0 && r < n && !isnan(sc)) {
-        key = make_key(sc, r);
+        key = row_key(sc, r);
         ++mine;
       }
     }
@@ -285,8 +303,8 @@ __global__ void __launch_bounds__(kSortThreads) rerank_select(const int32_t *row
   const int cnt = min(included_s, keep);
   for (int j = threadIdx.x; j < keep; j += blockDim.x) {
     if (j < cnt) {
-      idx[j] = (int32_t)(0xFFFFFFFFu - (uint32_t)(keys[j] & 0xFFFFFFFFull));
-      out[j] = key_score(keys[j]);
+      idx[j] = row_key_row(keys[j]);
+      out[j] = row_key_score(keys[j]);
     } else {
       idx[j] = -1;
       out[j] = -INFINITY;

@@ -27,7 +27,7 @@ def _brute(ens, X, rows, keep):
     entries.sort(key=lambda e: (-e[0], e[1]))
     sel = entries[:keep]
     idx = [r for _, r in sel] + [-1] * (keep - len(sel))
-    top = [abs(s) if s == 0 else s for s, _ in sel] + [-np.inf] * (keep - len(sel))
+    top = [s for s, _ in sel] + [-np.inf] * (keep - len(sel))
     return (np.array(scores, np.float32), np.array(idx, np.int32), np.array(top, np.float32),
             len(sel))
 
@@ -81,14 +81,18 @@ def test_rerank_padding_and_empty():
 
 
 def test_rerank_signed_zero():
-    # base -0.0 plus a -0.0 leaf folds to -0.0; it is reported as +0.0 and ties
-    # with a +0.0 score by row
+    # base -0.0 plus a -0.0 leaf folds to -0.0 (rows 0 and 2), base -0.0 plus a
+    # +0.0 leaf to +0.0 (row 1).  -0.0 and +0.0 are equal in the order, so the
+    # three tie and go by row; each kept entry reports its own score, sign of
+    # zero included (the selection returns the scores it ranked, as the
+    # top-k does).
     A = ensemble_from_trees([(0, 0.5, -0.0, 0.0)], num_features=1, base=-0.0)
     X = np.array([[0.0], [1.0], [0.0]], np.float32)  # rows 0, 2 -> -0.0; row 1 -> +0.0
     row_scores, idx, top, num = oracle.rerank(A, X, np.array([2, 1, 0], np.int32), 3)
     assert np.signbit(row_scores[0]) and not np.signbit(row_scores[1])
-    assert list(idx) == [0, 1, 2]
-    assert not np.any(np.signbit(top))
+    assert list(idx) == [0, 1, 2] and num == 3
+    assert list(np.signbit(top)) == [True, False, True]
+    assert np.all(top == 0.0)
 
 
 def test_rerank_order_is_score_then_row():
