@@ -34,20 +34,30 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0
 # Node-visit ceiling of the chip, from its unit counts and clock (256 CUs,
-# 2.4 GHz).  A visit needs, per lane, two VALU instructions (the comparison
-# x[feature] < threshold and the step to the chosen child) and two LDS reads
-# (the 8-byte node and the 4-byte feature value).
+# 2.4 GHz).  A visit needs, per lane, two LDS reads (the 8-byte node and the
+# 4-byte feature value) and, as counted on the walks (SQ_INSTS_VALU per
+# wave-visit: 5.01 in the perf walk, 5.27 in the validity walk), five VALU
+# instructions (node address, feature address, the comparison
+# x[feature] < threshold, the step to the chosen child, and the share of the
+# fold and of the staging).
 #   VALU: the fp32 vector peak of 157.3 TFLOP/s is 78.6 T lane-FMAs/s, i.e.
-#         128 lanes per clock per CU -> 39.3 T visits/s.
+#         128 lanes per clock per CU -> 78.6 T / 5 = 15.7 T visits/s.
 #   LDS:  256 bytes per clock per CU (CDNA4 doubled CDNA3's 128; the
-#         consecutive 16-byte read probe of --probe reaches 160 B/clk)
+#         consecutive 16-byte read probe of --probe reaches 156 B/clk)
 #         -> 157 TB/s / 12 B = 13.1 T visits/s.
-# The lower one, the LDS ceiling, is the peak.
+# The lower one, the LDS ceiling, is the peak.  Beside it the line carries
+# the walk loop's measured rate at the perf walk's shape (the probe of
+# --probe: the same loop over a resident chunk, no row loads or restaging).
 VALU_LANE_OPS_PER_S = 256 * 128 * 2.4e9
-VISIT_PEAK_VALU = VALU_LANE_OPS_PER_S / 2
+VALU_PER_VISIT = 5
+VISIT_PEAK_VALU = VALU_LANE_OPS_PER_S / VALU_PER_VISIT
 LDS_BYTES_PER_S = 256 * 256 * 2.4e9
 VISIT_PEAK_LDS = LDS_BYTES_PER_S / 12
 VISIT_PEAK_PER_S = min(VISIT_PEAK_VALU, VISIT_PEAK_LDS)
+MALL_BYTES = 256 << 20  # MI355X Infinity Cache: pools below it are flushed between steps
+# The perf walk's launch shape on the 16M pool (depth, trees per lane, lanes
+# per candidate, waves, features): the shape of the walk-loop probe.
+PERF_WALK_SHAPE = {"roofline": (8, 4, 2, 8, 128)}
 METRIC = "candidate configs scored+filtered/sec (validity+perf+top-k); % of HBM peak"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "perf_walk_roofline_traffic.json")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2411_10764_amd", "csrc", "walk_kernels.hip")
@@ -144,23 +154,57 @@ def mean_path(ens, X) -> float:
     return total / X.shape[0]
 
 
-def cpu_baseline(w, rows: int):
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def cpu_baseline(w, rows: int, rows_one: int):
+    """The oracle as it stands on the host cores: all usable threads on the
+    first `rows` candidates, and one thread on the first `rows_one`."""
     import gen
     import oracle
     threads = gen.default_threads()
     X = w.features(rows=np.arange(rows, dtype=np.int64))
     V, P = oracle.OracleEnsemble(w.validity()), oracle.OracleEnsemble(w.perf())
     A = oracle.OracleEnsemble(w.second_level()) if w.a_trees else None
-    t0 = time.perf_counter()
-    out = oracle.pipeline(V, P, X, w.k, threads=threads)
-    if A is not None:
-        oracle.rerank(A, X, out["idx"], w.keep)
-    dt = time.perf_counter() - t0
+
+    def run(Xs, t):
+        t0 = time.perf_counter()
+        out = oracle.pipeline(V, P, Xs, w.k, threads=t)
+        if A is not None:
+            oracle.rerank(A, Xs, out["idx"], w.keep)
+        return time.perf_counter() - t0
+
+    dt = run(X, threads)
+    dt1 = run(X[:rows_one], 1)
     steps = f"validity -> masked perf -> top-{w.k}" + (f" -> model A keeps {w.keep}" if A else "")
     return {"value": rows / dt, "unit": "candidates/s", "cores": threads, "kind": "oracle",
             "sample": f"first {rows} candidates of the {w.name} pool ({w.F} features), "
                       f"{steps}, {dt:.2f} s wall on {threads} threads "
-                      f"({os.cpu_count()} visible cpus)"}
+                      f"({os.cpu_count()} visible cpus)",
+            "single_core": {"value": rows_one / dt1, "unit": "candidates/s", "cores": 1,
+                            "sample": f"first {rows_one} candidates, the same steps, "
+                                      f"{dt1:.2f} s wall on one thread"},
+            "cpu_model": cpu_model()}
+
+
+def walk_loop_ceiling(shape):
+    """T visits/s of the walk's inner loop at `shape` (the --probe
+    microbenchmark, timed live on this device)."""
+    import torch
+    from paper_2411_10764_amd import ml2
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    d, g, s_, waves, f = shape
+    ms, visits = ml2.ml2_probe_visit(d, g, s_, waves, f, 512 if d == 8 else 1024, 4 * cus)
+    return visits / (ms * 1e-3) / 1e12
 
 
 def explore(args, w, X, v, p, dev) -> int:
@@ -253,6 +297,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="roofline")
     ap.add_argument("--cpu-rows", type=int, default=1 << 20)
+    ap.add_argument("--cpu-rows-one", type=int, default=1 << 17,
+                    help="candidates of the single-thread oracle timing")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-probe", action="store_true")
     ap.add_argument("--probe", action="store_true",
@@ -332,7 +378,16 @@ def main() -> int:
         if e is not None:
             e[4].record(stream)
 
+    # Pools that fit the 256 MB MALL are flushed before every step (a 512 MB
+    # read-modify-write on the same stream, outside the timed events), so
+    # that each step reads the pool from HBM.
+    flush = None
+    if 4.0 * w.F * w.n < MALL_BYTES:
+        flush = torch.zeros(2 * MALL_BYTES // 4, dtype=torch.float32, device=dev)
+
     for _ in range(args.warmup):
+        if flush is not None:
+            flush.add_(1.0)
         step()
     torch.cuda.synchronize()
     _log(f"warmup done ({args.warmup} steps)")
@@ -341,22 +396,27 @@ def main() -> int:
     torch.cuda.synchronize()
     start = time.perf_counter()
     for s in range(args.steps):
+        if flush is not None:
+            flush.add_(1.0)
         step(ev[s])
     torch.cuda.synchronize()
     wall = time.perf_counter() - start
-    t_val = np.mean([e[0].elapsed_time(e[1]) for e in ev])
-    t_perf = np.mean([e[1].elapsed_time(e[2]) for e in ev])
-    t_topk = np.mean([e[2].elapsed_time(e[3]) for e in ev])
-    t_rerank = np.mean([e[3].elapsed_time(e[4]) for e in ev])
-    t_step = np.mean([e[0].elapsed_time(e[4]) for e in ev])
-    ms_per_step = 1000.0 * wall / args.steps
+    # medians over the timed steps of the HIP-event durations on the stream
+    t_val = float(np.median([e[0].elapsed_time(e[1]) for e in ev]))
+    t_perf = float(np.median([e[1].elapsed_time(e[2]) for e in ev]))
+    t_topk = float(np.median([e[2].elapsed_time(e[3]) for e in ev]))
+    t_rerank = float(np.median([e[3].elapsed_time(e[4]) for e in ev]))
+    steps_ms = [e[0].elapsed_time(e[4]) for e in ev]
+    ms_per_step = float(np.median(steps_ms))
     valid = pipe.valid.cpu().numpy()
     n_valid = int(valid.sum())
     num = int(pipe.num.item())
-    _log(f"step {ms_per_step:.3f} ms (events {t_step:.3f}): validity {t_val:.3f} ms, "
-         f"perf {t_perf:.3f} ms, top-k {t_topk:.3f} ms"
+    _log(f"step {ms_per_step:.3f} ms (median of {args.steps}; mean {np.mean(steps_ms):.3f}, "
+         f"wall {1000.0 * wall / args.steps:.3f}{' with MALL flushes' if flush is not None else ''}):"
+         f" validity {t_val:.3f} ms, perf {t_perf:.3f} ms, top-k {t_topk:.3f} ms"
          + (f", re-rank {t_rerank:.3f} ms (kept {int(a_num.item())})" if second else "")
          + f"; valid {n_valid}/{w.n}, selected {num}")
+    del flush
 
     value = w.n / (ms_per_step / 1000.0)
     f_vp = w.K if w.visible_only else w.F
@@ -377,12 +437,17 @@ def main() -> int:
     if w.name == "hbm":
         return _print(out_hbm(w, args, value, ms_per_step, t_val, t_perf, t_topk, n_valid,
                               alg_bytes))
+    shape = PERF_WALK_SHAPE.get(w.name)
+    loop = walk_loop_ceiling(shape) * 1e12 if shape else None
     roofline = {
         "bound": "alu",
+        "limiter": "lds",
         "kernel": "perf_kernel (model P walk over accepted candidates)",
-        "peak_derivation": "node visits: LDS 256 B/clk/CU x 256 CU x 2.4 GHz / 12 B per visit "
-                           f"= {VISIT_PEAK_LDS / 1e12:.1f} T/s (VALU: 128 lanes/clk/CU / 2 "
-                           f"instructions per visit = {VISIT_PEAK_VALU / 1e12:.1f} T/s)",
+        "peak_derivation": "node visits on chip (LDS + VALU, no HBM or MFMA term): LDS 256 "
+                           "B/clk/CU x 256 CU x 2.4 GHz / 12 B per visit = "
+                           f"{VISIT_PEAK_LDS / 1e12:.1f} T/s; VALU 128 lanes/clk/CU x 256 CU x "
+                           f"2.4 GHz / {VALU_PER_VISIT} instructions per visit (counted) = "
+                           f"{VISIT_PEAK_VALU / 1e12:.1f} T/s; peak = the lower (LDS)",
         "achieved": perf_visits_per_s / 1e12,
         "peak": VISIT_PEAK_PER_S / 1e12,
         "unit": "Tvisit/s",
@@ -392,6 +457,13 @@ def main() -> int:
         "work_per_launch": f"{visits_p} node visits ({n_valid} accepted x {w.p_trees} trees "
                            + (f"x measured mean path)" if w.ragged else f"x depth {w.p_depth})"),
         "launch_ms": t_perf,
+        "measured_ceiling": ({"achieved": loop / 1e12,
+                              "frac": perf_visits_per_s / loop,
+                              "what": "walk loop alone at the perf walk's shape "
+                                      f"(depth {shape[0]}, {shape[1]} trees per lane, {shape[2]} "
+                                      f"lanes per candidate, {shape[3]} waves, {shape[4]} "
+                                      "features; ml2_probe_visit, timed live)"}
+                             if loop else None),
         "validity_kernel": {"achieved": visits_v / (t_val / 1000.0) / 1e12, "launch_ms": t_val,
                             "frac": visits_v / (t_val / 1000.0) / VISIT_PEAK_PER_S},
         "hbm": {"algorithmic_bytes_per_step": alg_bytes,
@@ -402,6 +474,8 @@ def main() -> int:
     out = {
         "metric": METRIC, "value": value, "unit": "candidates/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
+        "timing": "median of per-step HIP-event durations on the launch stream"
+                  + (", MALL flushed before each step" if 4.0 * w.F * w.n < MALL_BYTES else ""),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic (seeded knob + lognormal features, random perfect trees)",
         "config": {"workload": w.name, "candidates": w.n, "features": w.F,
@@ -422,7 +496,7 @@ def main() -> int:
     torch.cuda.empty_cache()
     if not args.no_cpu:
         _log(f"cpu baseline: oracle on {args.cpu_rows} candidates")
-        out["cpu_baseline"] = cpu_baseline(w, args.cpu_rows)
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_rows, args.cpu_rows_one)
     else:
         out["cpu_baseline"] = None
     print(json.dumps(out), flush=True)

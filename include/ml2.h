@@ -109,8 +109,10 @@ typedef struct {
  */
 ml2_status ml2_load_ensemble(const ml2_ensemble_desc *desc, ml2_ensemble **out);
 
-/* Release an ensemble (NULL is ignored).  Synchronises the device first, so
- * no work that uses it may still be pending. */
+/* Release an ensemble (NULL is ignored).  The caller must have finished
+ * every call that uses it (work enqueued on a stream counts until that
+ * stream has passed it).  The device memory is returned with hipFree, which
+ * waits for the device. */
 void ml2_free_ensemble(ml2_ensemble *e);
 
 /* Number of features / trees / depth (the longest path, or the padded depth
@@ -229,7 +231,8 @@ typedef struct ml2_explorer ml2_explorer;
 ml2_status ml2_explorer_create(const ml2_ensemble *v, const ml2_ensemble *p,
                                const ml2_ensemble *a, int64_t n, int32_t k, int32_t keep,
                                int32_t max_rounds, ml2_explorer **out);
-/* Waits for the device, then releases the explorer's memory (NULL is a no-op). */
+/* Releases the explorer's memory (NULL is a no-op); as ml2_free_ensemble, the
+ * caller must have finished every round enqueued on it. */
 void ml2_explorer_free(ml2_explorer *ex);
 /* Forgets every proposed row and the stored scores (INVALID_ARG if NULL). */
 ml2_status ml2_explorer_reset(ml2_explorer *ex);

@@ -399,17 +399,16 @@ ml2_status ml2_load_ensemble(const ml2_ensemble_desc *desc, ml2_ensemble **out) 
 
   // Layout: perfect padded trees where they represent the ensemble and are
   // not much larger than its nodes; ragged slots otherwise (deeper than the
-  // perfect limit, default directions, or sparse trees).  ML2_LAYOUT=ragged
-  // or =perfect forces a layout that can represent the ensemble.
+  // perfect limit, default directions, or sparse trees).  The tuning
+  // override (ml2_tune_layout) forces a layout that can represent it.
   const int64_t tpad16 = (d.num_trees + ml2::kTreePad - 1) / ml2::kTreePad * ml2::kTreePad;
   const bool perfect_ok = depth <= ml2::kMaxPerfectDepth && !any_default_left;
   const bool ragged_ok = max_nodes <= ML2_MAX_TREE_NODES;
   bool ragged = !perfect_ok ||
                 (ragged_ok && (double)tpad16 * ml2::record_bytes(depth) > 4.0 * 12.0 * total_nodes);
-  if (const char *lay = getenv("ML2_LAYOUT")) {
-    if (!strcmp(lay, "ragged") && ragged_ok) ragged = true;
-    if (!strcmp(lay, "perfect") && perfect_ok) ragged = false;
-  }
+  const int forced = ml2::get_tune(ml2::kTuneLayout);
+  if (forced == 2 && ragged_ok) ragged = true;
+  if (forced == 1 && perfect_ok) ragged = false;
   if (ragged && !ragged_ok)
     return fail(ML2_ERR_UNSUPPORTED,
                 "a tree of %lld nodes needs the ragged layout (deeper than %d levels or default "
@@ -482,15 +481,10 @@ ml2_status ml2_load_ensemble(const ml2_ensemble_desc *desc, ml2_ensemble **out) 
 void ml2_free_ensemble(ml2_ensemble *e) {
   if (!e) return;
   int cur = 0;
-  if (hipGetDevice(&cur) == hipSuccess && cur != e->f.device) {
-    (void)hipSetDevice(e->f.device);
-    (void)hipDeviceSynchronize();
-    (void)hipFree(e->f.d_trees);
-    (void)hipSetDevice(cur);
-  } else {
-    (void)hipDeviceSynchronize();
-    (void)hipFree(e->f.d_trees);
-  }
+  const bool other = hipGetDevice(&cur) == hipSuccess && cur != e->f.device;
+  if (other) (void)hipSetDevice(e->f.device);
+  (void)hipFree(e->f.d_trees);
+  if (other) (void)hipSetDevice(cur);
   delete e;
 }
 
@@ -686,7 +680,6 @@ void ml2_explorer_free(ml2_explorer *ex) {
   int cur = 0;
   const bool other = hipGetDevice(&cur) == hipSuccess && cur != ex->device;
   if (other) (void)hipSetDevice(ex->device);
-  (void)hipDeviceSynchronize();
   (void)hipFree(ex->block);
   if (other) (void)hipSetDevice(cur);
   delete ex;
@@ -754,6 +747,30 @@ ml2_status ml2_explorer_round(ml2_explorer *ex, const float *X, int64_t ld, int3
   if (e != hipSuccess) return hip_fail(e, "explorer selection launch");
   ex->rounds += 1;
   ex->scored = true;
+  return ML2_OK;
+}
+
+// ---- tuning overrides (ml2_probe.h) ------------------------------------------
+
+ml2_status ml2_tune_walk_plan(int32_t split, int32_t group, int32_t waves, int32_t nbuf,
+                              int32_t chunk) {
+  if (split < 0 || split > 2 || group < 0 || group > 16 || waves < 0 || waves > 8 || nbuf < 0 ||
+      nbuf > 2 || chunk < 0 || chunk > 4096)
+    return fail(ML2_ERR_INVALID_ARG,
+                "ml2_tune_walk_plan: split %d, group %d, waves %d, nbuf %d, chunk %d out of range",
+                split, group, waves, nbuf, chunk);
+  ml2::set_tune(ml2::kTuneSplit, split);
+  ml2::set_tune(ml2::kTuneGroup, group);
+  ml2::set_tune(ml2::kTuneWaves, waves);
+  ml2::set_tune(ml2::kTuneNbuf, nbuf);
+  ml2::set_tune(ml2::kTuneChunk, chunk);
+  return ML2_OK;
+}
+
+ml2_status ml2_tune_layout(int32_t layout) {
+  if (layout < 0 || layout > 2)
+    return fail(ML2_ERR_INVALID_ARG, "ml2_tune_layout: layout = %d outside [0, 2]", layout);
+  ml2::set_tune(ml2::kTuneLayout, layout);
   return ML2_OK;
 }
 

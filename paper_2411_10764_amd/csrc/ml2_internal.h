@@ -88,6 +88,13 @@ struct WalkPlan {
 // Returns false (and sets *why) if no plan fits the LDS of one workgroup.
 bool plan_walk(const Forest &f, int64_t n_work, int cu_count, WalkPlan *plan, const char **why);
 
+// Tuning overrides (ml2_tune_walk_plan / ml2_tune_layout): process-wide,
+// zero = the planner's or loader's choice.
+enum TuneField { kTuneSplit, kTuneGroup, kTuneWaves, kTuneNbuf, kTuneChunk, kTuneLayout,
+                 kTuneFields };
+void set_tune(int field, int value);
+int get_tune(int field);
+
 hipError_t launch_validity(const Forest &f, const WalkPlan &p, const float *X, int64_t n,
                            int64_t ld, uint8_t *valid_out, float *margin_out, hipStream_t s);
 hipError_t launch_perf(const Forest &f, const WalkPlan &p, const float *X, int64_t n,

@@ -38,6 +38,7 @@
 #include <stdlib.h>
 
 #include <algorithm>
+#include <atomic>
 #include <type_traits>
 
 #include "ml2_internal.h"
@@ -1446,10 +1447,7 @@ hipError_t launch_leaves(int depth, const WalkArgs &a, int G, int W, size_t lds,
   }
 }
 
-int env_int(const char *name, int dflt) {
-  const char *v = getenv(name);
-  return (v && *v) ? atoi(v) : dflt;
-}
+std::atomic<int> g_tune[kTuneFields];
 
 size_t stage_reg_bytes(const WalkPlan &p) {
   return (size_t)(6 / p.split) * 16 * kLanes * p.waves;
@@ -1523,6 +1521,9 @@ bool try_plan(const Forest &f, int64_t n_work, int cu_count, int S, int W, int m
 
 }  // namespace
 
+void set_tune(int field, int value) { g_tune[field].store(value, std::memory_order_relaxed); }
+int get_tune(int field) { return g_tune[field].load(std::memory_order_relaxed); }
+
 // LDS of one workgroup = W candidate tiles (F * 256 / S bytes each, plus the
 // compaction queue share) + nbuf chunk buffers of chunk_trees whole trees
 // (a multiple of S*G, as large as the LDS allows).  Preference: eight waves
@@ -1530,15 +1531,15 @@ bool try_plan(const Forest &f, int64_t n_work, int cu_count, int S, int W, int m
 // (twice the candidates per pass over the ensemble), else two; then one lane
 // per candidate with four waves in the order register staging, two buffers,
 // synchronous copy; then fewer waves.  Larger G first within each (ragged
-// trees with one lane per candidate: smaller G first).  ML2_WALK_SPLIT /
-// ML2_WALK_GROUP / ML2_WALK_WAVES / ML2_WALK_NBUF / ML2_WALK_CHUNK override
-// the choice (tuning sweeps); overrides that do not fit are ignored.
+// trees with one lane per candidate: smaller G first).  The tuning overrides
+// (ml2_tune_walk_plan) replace the choice where they fit; overrides that do
+// not fit are ignored.
 bool plan_walk(const Forest &f, int64_t n_work, int cu_count, WalkPlan *p, const char **why) {
-  const int want_s = env_int("ML2_WALK_SPLIT", 0);
-  const int want_g = env_int("ML2_WALK_GROUP", 0);
-  const int want_w = env_int("ML2_WALK_WAVES", 0);
-  const int want_b = env_int("ML2_WALK_NBUF", 0);
-  const int want_c = env_int("ML2_WALK_CHUNK", 0);
+  const int want_s = get_tune(kTuneSplit);
+  const int want_g = get_tune(kTuneGroup);
+  const int want_w = get_tune(kTuneWaves);
+  const int want_b = get_tune(kTuneNbuf);
+  const int want_c = get_tune(kTuneChunk);
   const int groups[5] = {16, 8, 4, 2, 1};
   // ragged trees with one lane per candidate: one tree per lane first (each
   // lane then moves to its next tree as soon as its walk is on a leaf, and

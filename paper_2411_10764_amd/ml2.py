@@ -35,7 +35,8 @@ EXPORTED = (
     "ml2_explorer_round", "ml2_last_error",
 )
 # include/ml2_probe.h: microbenchmarks behind the roofline figures
-EXPORTED_PROBE = ("ml2_probe_visit", "ml2_probe_lds", "ml2_probe_valu")
+EXPORTED_PROBE = ("ml2_probe_visit", "ml2_probe_lds", "ml2_probe_valu", "ml2_tune_walk_plan",
+                  "ml2_tune_layout")
 
 
 class Ml2Error(RuntimeError):
@@ -109,6 +110,10 @@ def lib():
         L.ml2_probe_lds.argtypes = [I32, I32, I32, D, D]
         L.ml2_probe_valu.restype = I32
         L.ml2_probe_valu.argtypes = [I32, I32, D, D]
+        L.ml2_tune_walk_plan.restype = I32
+        L.ml2_tune_walk_plan.argtypes = [I32, I32, I32, I32, I32]
+        L.ml2_tune_layout.restype = I32
+        L.ml2_tune_layout.argtypes = [I32]
         _lib = L
     return _lib
 
@@ -352,3 +357,18 @@ def ml2_probe_lds(mode: int, iters: int, blocks: int):
 def ml2_probe_valu(iters: int, blocks: int):
     """(ms, lane additions) of chains of 32-bit adds."""
     return _probe(lib().ml2_probe_valu, iters, blocks)
+
+
+# ---- tuning overrides (include/ml2_probe.h) --------------------------------
+
+def ml2_tune_walk_plan(split: int = 0, group: int = 0, waves: int = 0, nbuf: int = 0,
+                       chunk: int = 0) -> None:
+    """Force the walks' launch shape for every later call (zeros: the
+    planner's choice); results are unchanged, only the shape differs."""
+    _check(lib().ml2_tune_walk_plan(split, group, waves, nbuf, chunk))
+
+
+def ml2_tune_layout(layout: int = 0) -> None:
+    """Force the layout of later loads: 0 the loader's choice, 1 perfect,
+    2 ragged (where the ensemble allows it)."""
+    _check(lib().ml2_tune_layout(layout))

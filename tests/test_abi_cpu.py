@@ -60,6 +60,26 @@ def test_probe_argument_errors(call):
     assert ms.value == -1.0 and w.value == -1.0
 
 
+@pytest.mark.parametrize("args", [(-1, 0, 0, 0, 0), (3, 0, 0, 0, 0), (0, 17, 0, 0, 0),
+                                  (0, 0, 9, 0, 0), (0, 0, 0, 3, 0), (0, 0, 0, 0, -4)])
+def test_tune_walk_plan_argument_errors(args):
+    """The launch-plan override rejects out-of-range fields and leaves the
+    current override unchanged (no GPU needed: it only records the fields)."""
+    L = ml2.lib()
+    assert L.ml2_tune_walk_plan(*args) == ml2.ML2_ERR_INVALID_ARG
+    assert "ml2_tune_walk_plan" in L.ml2_last_error().decode()
+    assert L.ml2_tune_walk_plan(2, 4, 8, 1, 16) == ml2.ML2_OK
+    assert L.ml2_tune_walk_plan(0, 0, 0, 0, 0) == ml2.ML2_OK
+
+
+def test_tune_layout_argument_errors():
+    L = ml2.lib()
+    for bad in (-1, 3):
+        assert L.ml2_tune_layout(bad) == ml2.ML2_ERR_INVALID_ARG
+    for good in (1, 2, 0):
+        assert L.ml2_tune_layout(good) == ml2.ML2_OK
+
+
 def test_header_constants_match_binding():
     text = open(HEADER).read()
     for name in ("ML2_MAX_DEPTH", "ML2_MAX_TREE_NODES", "ML2_MAX_FEATURES", "ML2_MAX_TOPK"):

@@ -25,13 +25,31 @@ def test_more_than_one_gpu_is_refused(gpus):
 
 def test_visit_ceiling_from_unit_counts():
     # 256 CUs at 2.4 GHz: LDS 256 B/clk/CU over 12 B per visit, VALU 128
-    # lanes/clk/CU over 2 instructions per visit; the lower one is the peak.
+    # lanes/clk/CU over the 5 instructions per visit counted on the walks
+    # (SQ_INSTS_VALU per wave-visit 5.01 / 5.27); the lower one is the peak.
     lds = 256 * 256 * 2.4e9 / 12
-    valu = 256 * 128 * 2.4e9 / 2
+    valu = 256 * 128 * 2.4e9 / 5
     assert bench.VISIT_PEAK_LDS == pytest.approx(lds)
     assert bench.VISIT_PEAK_VALU == pytest.approx(valu)
+    assert bench.VISIT_PEAK_VALU == pytest.approx(15.72864e12)
     assert bench.VISIT_PEAK_PER_S == pytest.approx(min(lds, valu))
     assert bench.VISIT_PEAK_PER_S == pytest.approx(13.1072e12)
+
+
+def test_probe_shape_is_the_perf_walk_shape():
+    # the walk-loop ceiling is taken at the 16M pool's perf walk shape:
+    # depth 8, four trees per lane, two lanes per candidate, eight waves,
+    # 128 features
+    import gen
+    w = gen.WORKLOADS["roofline"]
+    d, g, s, waves, f = bench.PERF_WALK_SHAPE["roofline"]
+    assert d == w.p_depth and f == w.F and (g, s, waves) == (4, 2, 8)
+
+
+def test_mall_flush_applies_to_pools_below_the_cache():
+    import gen
+    small = [n for n, w in gen.WORKLOADS.items() if 4.0 * w.F * w.n < bench.MALL_BYTES]
+    assert sorted(small) == ["medium", "tiny"]
 
 
 def test_traffic_only_for_the_profiled_source(tmp_path, monkeypatch):

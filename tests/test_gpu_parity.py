@@ -205,12 +205,12 @@ def test_depth_and_width_limits(depth, F, trees):
     (2, 8, 8, 1, 0, 7), (2, 4, 8, 1, 16, 7), (2, 4, 4, 1, 0, 7), (2, 8, 8, 1, 32, 7),
     (2, 4, 8, 1, 16, 6), (2, 2, 8, 1, 0, 8), (2, 1, 8, 1, 0, 9), (2, 1, 8, 1, 0, 10),
 ])
-def test_walk_plans(monkeypatch, split, group, waves, nbuf, chunk, depth):
+def test_walk_plans(tune, split, group, waves, nbuf, chunk, depth):
     """Every launch shape of the walks (lanes per candidate, trees per lane,
     waves, staging mode, chunk size), forced through the tuning overrides."""
     for key, val in (("SPLIT", split), ("GROUP", group), ("WAVES", waves), ("NBUF", nbuf),
                      ("CHUNK", chunk)):
-        monkeypatch.setenv(f"ML2_WALK_{key}", str(val))
+        tune(**{key.lower(): val})
     F, K = 40, 20
     V = gen.perfect_ensemble(31, 1, 70, depth, F, K, 0.5)
     P = gen.perfect_ensemble(31, 2, 90, depth, F, K, 0.1)
@@ -220,7 +220,7 @@ def test_walk_plans(monkeypatch, split, group, waves, nbuf, chunk, depth):
 
 
 @pytest.mark.parametrize("seed", range(12))
-def test_perfect_random_shapes(monkeypatch, seed):
+def test_perfect_random_shapes(tune, seed):
     """Seeded random perfect ensembles (depth 1..12), feature counts, row
     strides and alignment, pool sizes and launch plans (overrides that do not
     fit are ignored by the planner), each against the oracle."""
@@ -235,7 +235,7 @@ def test_perfect_random_shapes(monkeypatch, seed):
                          ("NBUF", [0, 1, 2]), ("CHUNK", [0, 0, 16, 32])):
         val = int(rng.choice(choices))
         if val:
-            monkeypatch.setenv(f"ML2_WALK_{key}", str(val))
+            tune(**{key.lower(): val})
     tv = int(rng.integers(1, 80)) if depth <= 9 else int(rng.integers(1, 12))
     tp = int(rng.integers(1, 80)) if depth <= 9 else int(rng.integers(1, 12))
     V = gen.perfect_ensemble(4000 + seed, 1, tv, depth, F, K, 0.5, float(rng.normal(0, 0.3)))
@@ -249,11 +249,11 @@ def test_perfect_random_shapes(monkeypatch, seed):
 
 @pytest.mark.parametrize("F,ld,trees", [(40, 40, 30), (128, 128, 48), (128, 131, 20),
                                          (132, 132, 16), (6, 6, 1)])
-def test_resident_ensemble(monkeypatch, F, ld, trees):
+def test_resident_ensemble(tune, F, ld, trees):
     """Ensembles that fit one chunk (never restaged) with two lanes per
     candidate: rows prefetched whole into the staging registers where they
     are aligned and at most 128 wide, loaded directly otherwise."""
-    monkeypatch.setenv("ML2_WALK_SPLIT", "2")
+    tune(split=2)
     K = max(F // 2, 1)
     V = gen.perfect_ensemble(33, 1, trees, 5, F, K, 0.5)
     P = gen.perfect_ensemble(33, 2, trees, 4, F, K, 0.1)
@@ -263,11 +263,11 @@ def test_resident_ensemble(monkeypatch, F, ld, trees):
 
 
 @pytest.mark.parametrize("F", [72, 96, 124, 128])
-def test_row_widths_two_lanes(monkeypatch, F):
+def test_row_widths_two_lanes(tune, F):
     """Two lanes per candidate with the ensemble streamed in several chunks:
     row widths whose last line-batch is partial (the validity walk's halves
     share each line, the perf walk's halves take alternate lines)."""
-    monkeypatch.setenv("ML2_WALK_SPLIT", "2")
+    tune(split=2)
     K = F // 2
     V = gen.perfect_ensemble(34, 1, 160, 6, F, K, 0.5)
     P = gen.perfect_ensemble(34, 2, 120, 7, F, K, 0.1)
@@ -371,11 +371,37 @@ def test_repeatable_across_streams():
         assert np.array_equal(a.view(np.uint8), b.view(np.uint8))
 
 
-# ---- full-size workloads: sampled outputs + properties -----------------------------
+# ---- full-size workloads: every row against the oracle ------------------------------
+
+def _second_level_check(w, X, Xd, idx, num):
+    """Model A over the GPU's held rows, on the GPU and in the oracle."""
+    A = w.second_level()
+    a = ml2.ml2_load_ensemble(A)
+    m = w.k
+    rows = torch.from_numpy(idx.astype(np.int32)).to(DEV)
+    row_scores = torch.empty(m, dtype=torch.float32, device=DEV)
+    out_idx = torch.empty(w.keep, dtype=torch.int32, device=DEV)
+    out_top = torch.empty(w.keep, dtype=torch.float32, device=DEV)
+    out_num = torch.empty(1, dtype=torch.int32, device=DEV)
+    wsb = ml2.ml2_rerank_workspace_bytes(a, m)
+    ws = torch.empty(wsb, dtype=torch.uint8, device=DEV)
+    ml2.ml2_rerank(a, Xd, rows, w.keep, row_scores, out_idx, out_top, out_num, ws, wsb, m=m)
+    torch.cuda.synchronize()
+    o_rs, o_idx, o_top, o_num = oracle.rerank(A, X, idx.astype(np.int32), w.keep)
+    assert_scores(row_scores.cpu().numpy(), o_rs, "model A scores of the held rows")
+    assert int(out_num.item()) == o_num
+    assert np.array_equal(out_idx.cpu().numpy(), o_idx), "model A's kept rows differ"
+    assert np.array_equal(out_top.cpu().numpy().view(np.uint32), o_top.view(np.uint32))
+    a.free()
+
 
 @pytest.mark.slow
-@pytest.mark.parametrize("name", ["large", "roofline", "skewed", "hbm", "paper"])
-def test_full_size_sampled(name):
+@pytest.mark.parametrize("name", ["large", "roofline", "skewed", "hbm", "paper", "explorer"])
+def test_full_size_whole_pool(name):
+    """Every row of the full-size pool against the oracle: mask bytes,
+    margins and scores bit for bit, and the top-k (indices, scores, count)
+    equal to the oracle's selection over the oracle's own scores."""
+    import time
     w = gen.WORKLOADS[name]
     _note(f"{name}: generating {w.n} x {w.F} features on the host")
     X = w.features()
@@ -392,32 +418,25 @@ def test_full_size_sampled(name):
     idx = pipe.idx.cpu().numpy()[: w.k]
     top = pipe.top.cpu().numpy()[: w.k]
     num = int(pipe.num.item())
-    del Xd
-    rng = np.random.default_rng(w.seed)
-    rows = np.unique(np.concatenate([rng.choice(w.n, 40000, replace=False),
-                                     np.arange(0, 70), np.arange(w.n - 70, w.n),
-                                     idx[idx >= 0]])).astype(np.int64)
-    _note(f"{name}: oracle on {rows.size} sampled rows")
-    Xs = X[rows]
-    ov, om = oracle.validity(V, Xs, THREADS)
-    os_ = oracle.perf(P, Xs, ov, THREADS)
-    assert np.array_equal(valid[rows], ov), "validity mask differs on sampled rows"
-    assert_scores(margin[rows], om, "margin (sampled)")
-    assert_scores(score[rows], os_, "score (sampled)")
-    # top-k properties over the whole pool (the selected rows were checked above)
-    n_valid = int(valid.sum())
-    assert num == min(w.k, n_valid)
-    sel = idx[:num]
-    assert len(set(sel.tolist())) == num and np.all(valid[sel] == 1)
-    assert np.array_equal(top[:num].view(np.uint32), score[sel].view(np.uint32))
-    keys = [(-float(score[i]), int(i)) for i in sel]
-    assert keys == sorted(keys)
-    last_s, last_i = float(score[sel[-1]]), int(sel[-1])
-    better = (valid == 1) & ((score > last_s) | ((score == last_s) & (np.arange(w.n) <= last_i)))
-    assert int(better.sum()) == num, "a better valid candidate was left out"
-    _note(f"{name}: invalid fraction {1 - n_valid / w.n:.4f}; sampled rows exact; top-{w.k} ok")
     v.free()
     p.free()
+    _note(f"{name}: oracle on all {w.n} rows ({THREADS} threads)")
+    t0 = time.perf_counter()
+    ov, om = oracle.validity(V, X, THREADS)
+    os_ = oracle.perf(P, X, ov, THREADS)
+    oidx, otop, onum = oracle.topk(ov, os_, w.k)
+    _note(f"{name}: oracle took {time.perf_counter() - t0:.1f} s")
+    assert np.array_equal(valid, ov), f"validity mask differs on {int((valid != ov).sum())} rows"
+    assert_scores(margin, om, "margin")
+    assert_scores(score, os_, "score")
+    assert num == onum
+    assert np.array_equal(idx, oidx), "top-k indices differ"
+    assert np.array_equal(top.view(np.uint32), otop.view(np.uint32)), "top-k scores differ"
+    if w.a_trees:
+        _second_level_check(w, X, Xd, idx, num)
+    del Xd
+    _note(f"{name}: invalid fraction {1 - int(ov.sum()) / w.n:.4f}; every row and the "
+          f"top-{w.k} identical to the oracle")
 
 
 # ---- one GPU's share and the merge of shards ---------------------------------------
@@ -465,6 +484,13 @@ def test_shard_merge_matches_whole():
     assert np.array_equal(got_idx, whole.idx[:num].cpu().numpy().astype(np.int64))
     assert np.array_equal(merged.top[:num].cpu().numpy().view(np.uint32),
                           whole.top[:num].cpu().numpy().view(np.uint32))
-    _note(f"shard merge: shards {np.diff(bounds).tolist()}; merged top-{k} identical")
+    ov, _ = oracle.validity(w.validity(), X, THREADS)
+    os_ = oracle.perf(w.perf(), X, ov, THREADS)
+    oidx, otop, onum = oracle.topk(ov, os_, k)
+    assert onum == num
+    assert np.array_equal(got_idx, oidx.astype(np.int64)), "merged top-k differs from the oracle's"
+    assert np.array_equal(merged.top[:num].cpu().numpy().view(np.uint32), otop.view(np.uint32))
+    _note(f"shard merge: shards {np.diff(bounds).tolist()}; merged top-{k} identical to the "
+          "undivided share's and to the oracle's")
     v.free()
     p.free()

@@ -74,12 +74,12 @@ def test_paper_shaped_pipeline_with_missing_values():
 @pytest.mark.parametrize("split,waves,nbuf,group", [
     (1, 4, 1, 0), (1, 8, 1, 0), (2, 8, 1, 0), (1, 4, 2, 0), (2, 4, 1, 0), (1, 2, 1, 0),
     (1, 8, 1, 1), (1, 8, 1, 2), (1, 4, 2, 4), (2, 8, 1, 1), (2, 8, 1, 2)])
-def test_ragged_plans(monkeypatch, split, waves, nbuf, group):
+def test_ragged_plans(tune, split, waves, nbuf, group):
     """Launch shapes of the ragged walks; group 0 leaves the trees per lane
     to the planner."""
     for key, val in (("SPLIT", split), ("WAVES", waves), ("NBUF", nbuf), ("GROUP", group)):
         if val:
-            monkeypatch.setenv(f"ML2_WALK_{key}", str(val))
+            tune(**{key.lower(): val})
     n, F, K = 3000, 40, 20
     V = gen.ragged_ensemble(63, 1, 60, 9, F, K, 0.5, base_score=0.2, max_nodes=300)
     P = gen.ragged_ensemble(63, 2, 90, 14, F, K, 0.1, max_nodes=300)
@@ -89,7 +89,7 @@ def test_ragged_plans(monkeypatch, split, waves, nbuf, group):
 
 
 @pytest.mark.parametrize("split,group", [(0, 0), (1, 2), (1, 4), (2, 0), (2, 1)])
-def test_ragged_shallow_trees(monkeypatch, split, group):
+def test_ragged_shallow_trees(tune, split, group):
     """Shallow trees (one to three splits; walks that end after a step or
     two, lanes that run through a slot's trees in a few steps, single-leaf
     padding trees after P's 37), V a slot of exactly four trees; the default
@@ -97,7 +97,7 @@ def test_ragged_shallow_trees(monkeypatch, split, group):
     candidate."""
     for key, val in (("SPLIT", split), ("GROUP", group)):
         if val:
-            monkeypatch.setenv(f"ML2_WALK_{key}", str(val))
+            tune(**{key.lower(): val})
     n, F, K = 2500, 24, 12
     V = gen.ragged_ensemble(66, 1, 4, 3, F, K, 0.5, base_score=0.1, p_split=0.3)
     P = gen.ragged_ensemble(66, 2, 37, 6, F, K, 0.1, p_split=0.3, decay=0.5)
@@ -108,10 +108,10 @@ def test_ragged_shallow_trees(monkeypatch, split, group):
 
 
 @pytest.mark.parametrize("split", [1, 2])
-def test_ragged_widest_rows(monkeypatch, split):
+def test_ragged_widest_rows(tune, split):
     """256 features: the node word's feature byte offset reaches 255 x 256
     (one lane per candidate) and its half (two lanes per candidate)."""
-    monkeypatch.setenv("ML2_WALK_SPLIT", str(split))
+    tune(split=split)
     n, F, K = 1500, 256, 128
     V = gen.ragged_ensemble(67, 1, 20, 9, F, K, 0.5, base_score=0.1, max_nodes=200)
     P = gen.ragged_ensemble(67, 2, 30, 12, F, K, 0.1, max_nodes=300)
@@ -123,7 +123,7 @@ def test_ragged_widest_rows(monkeypatch, split):
 
 
 @pytest.mark.parametrize("seed", range(12))
-def test_ragged_random_shapes(monkeypatch, seed):
+def test_ragged_random_shapes(tune, seed):
     """Seeded random ragged ensembles, feature counts, pool sizes (ragged
     tails), missing fractions and launch shapes (lanes per candidate, trees
     per lane), each against the oracle."""
@@ -135,7 +135,7 @@ def test_ragged_random_shapes(monkeypatch, seed):
     group = int(rng.choice([0, 1, 2, 4])) if split != 2 else int(rng.choice([0, 1, 2]))
     for key, val in (("SPLIT", split), ("GROUP", group)):
         if val:
-            monkeypatch.setenv(f"ML2_WALK_{key}", str(val))
+            tune(**{key.lower(): val})
     V = gen.ragged_ensemble(2000 + seed, 1, int(rng.integers(1, 60)), int(rng.integers(1, 16)),
                             F, K, 0.5, base_score=float(rng.normal(0, 0.5)),
                             p_split=float(rng.uniform(0.5, 1.0)), max_nodes=int(rng.integers(3, 600)))
@@ -149,9 +149,9 @@ def test_ragged_random_shapes(monkeypatch, seed):
     check_pipeline(V, P, X, k)
 
 
-def test_forced_ragged_layout_on_perfect_trees(monkeypatch):
+def test_forced_ragged_layout_on_perfect_trees(tune):
     """Perfect trees packed into ragged slots give the same results."""
-    monkeypatch.setenv("ML2_LAYOUT", "ragged")
+    tune(layout=2)
     w = gen.WORKLOADS["tiny"]
     check_pipeline(w.validity(), w.perf(), w.features(), w.k)
 
