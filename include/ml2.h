@@ -175,6 +175,26 @@ ml2_status ml2_filter_topk(const uint8_t *valid, const float *scores, int64_t n,
                            void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * ml2_filter_topk for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same selection and outputs as ml2_filter_topk, with the workspace
+ * taken from a static array in the library's device code instead of an
+ * argument.  The array (147,712 bytes, the workspace of k = ML2_MAX_TOPK) is
+ * held by each device the library runs on until the process ends; its
+ * device address is looked up on the first call on a device.  This call
+ * allocates nothing.
+ * Calls on one device share that device's array: two calls whose work
+ * overlaps on the device (on different streams, or from different threads,
+ * without ordering between them) race and give wrong results; calls ordered
+ * on one stream are safe.  Each call starts by clearing the state it uses.
+ * Arguments and errors as ml2_filter_topk without the workspace;
+ * UNSUPPORTED for k > ML2_MAX_TOPK (beyond the static array).
+ */
+ml2_status ml2_filter_topk_noalloc(const uint8_t *valid, const float *scores, int64_t n,
+                                   int32_t k, int32_t *topk_idx, float *topk_score,
+                                   int32_t *num_selected, void *stream);
+
+/*
  * Second-level selection (model A, Section 2 "Hidden Feature Extractor & ML
  * Model A"): of the (alpha+1)*N configurations the explorer holds, model A,
  * which sees the hidden features as well as the visible ones, picks the N

@@ -564,6 +564,39 @@ ml2_status ml2_filter_topk(const uint8_t *valid, const float *scores, int64_t n,
   return ML2_OK;
 }
 
+ml2_status ml2_filter_topk_noalloc(const uint8_t *valid, const float *scores, int64_t n,
+                                   int32_t k, int32_t *topk_idx, float *topk_score,
+                                   int32_t *num_selected, void *stream) {
+  if (n < 0 || n > (int64_t)INT32_MAX)
+    return fail(ML2_ERR_INVALID_ARG, "ml2_filter_topk_noalloc: n = %lld out of range",
+                (long long)n);
+  if (k < 0) return fail(ML2_ERR_INVALID_ARG, "ml2_filter_topk_noalloc: k = %d < 0", k);
+  if (k > ML2_MAX_TOPK)
+    return fail(ML2_ERR_UNSUPPORTED,
+                "ml2_filter_topk_noalloc: k = %d > %d (the static scratch holds the workspace "
+                "of k <= %d)", k, ML2_MAX_TOPK, ML2_MAX_TOPK);
+  if (!num_selected)
+    return fail(ML2_ERR_INVALID_ARG, "ml2_filter_topk_noalloc: num_selected is NULL");
+  if (n > 0 && !scores)
+    return fail(ML2_ERR_INVALID_ARG, "ml2_filter_topk_noalloc: scores is NULL");
+  if (k > 0 && (!topk_idx || !topk_score))
+    return fail(ML2_ERR_INVALID_ARG, "ml2_filter_topk_noalloc: NULL output array");
+  const size_t need = ml2::topk_workspace_bytes(n, k);
+  if (need > ml2::static_scratch_bytes())
+    return fail(ML2_ERR_UNSUPPORTED, "ml2_filter_topk_noalloc: workspace %zu > static %zu bytes",
+                need, ml2::static_scratch_bytes());
+  int dev = 0;
+  ml2_status st = current_device(&dev);
+  if (st != ML2_OK) return st;
+  void *ws = nullptr;
+  hipError_t e = ml2::static_scratch(dev, &ws);
+  if (e != hipSuccess) return hip_fail(e, "ml2_filter_topk_noalloc: hipGetSymbolAddress");
+  e = ml2::launch_topk(valid, scores, n, k, topk_idx, topk_score, num_selected, ws, cu_count(dev),
+                       static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "top-k kernel launch");
+  return ML2_OK;
+}
+
 ml2_status ml2_rerank_workspace_bytes(const ml2_ensemble *a, int32_t m, size_t *bytes) {
   if (!a || !bytes) return fail(ML2_ERR_INVALID_ARG, "ml2_rerank_workspace_bytes: NULL argument");
   if (m < 0) return fail(ML2_ERR_INVALID_ARG, "ml2_rerank_workspace_bytes: m = %d < 0", m);

@@ -108,6 +108,11 @@ hipError_t launch_rows(const Forest &f, const float *X, int64_t n, int64_t ld, c
                        int32_t m, float *score_out, void *ws, int cu_count, hipStream_t s);
 
 size_t topk_workspace_bytes(int64_t n, int32_t k);
+// Device address of the selection's static scratch on `device` (which must
+// be current), looked up once per device; its size covers any k up to
+// ML2_MAX_TOPK.
+size_t static_scratch_bytes();
+hipError_t static_scratch(int device, void **ptr);
 hipError_t launch_topk(const uint8_t *valid, const float *scores, int64_t n, int32_t k,
                        int32_t *idx, float *score, int32_t *num, void *ws, int cu_count,
                        hipStream_t s);

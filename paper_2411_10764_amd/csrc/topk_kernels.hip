@@ -15,6 +15,9 @@
 // once when the selection is already complete, so the host never waits.
 #include <math.h>
 
+#include <mutex>
+#include <vector>
+
 #include "ml2_internal.h"
 
 namespace ml2 {
@@ -329,6 +332,35 @@ size_t topk_workspace_bytes(int64_t n, int32_t k) {
   (void)n;
   const size_t cand = (size_t)(k > 0 ? k : 1) * sizeof(unsigned long long);
   return (kStateBytes + kHistBytes + cand + 255) & ~(size_t)255;
+}
+
+// The selection's workspace for callers that cannot allocate
+// (ml2_filter_topk_noalloc): one file-scope array per device, sized for the
+// largest k, shared by every such call on that device.  Host code never
+// passes `scratch` itself to a kernel (on the host it only names the
+// symbol); it uses the device address hipGetSymbolAddress returns, taken
+// once per device with that device current.
+constexpr size_t kStaticScratchBytes =
+    (kStateBytes + kHistBytes + (size_t)ML2_MAX_TOPK * sizeof(unsigned long long) + 255) &
+    ~(size_t)255;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+size_t static_scratch_bytes() { return kStaticScratchBytes; }
+
+hipError_t static_scratch(int device, void **ptr) {
+  static std::mutex mu;
+  static std::vector<void *> addr;
+  std::lock_guard<std::mutex> lock(mu);
+  if ((int)addr.size() <= device) addr.resize((size_t)device + 1, nullptr);
+  if (!addr[(size_t)device]) {
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p || (reinterpret_cast<uintptr_t>(p) & 255u)) return hipErrorInvalidSymbol;
+    addr[(size_t)device] = p;
+  }
+  *ptr = addr[(size_t)device];
+  return hipSuccess;
 }
 
 hipError_t launch_topk(const uint8_t *valid, const float *scores, int64_t n, int32_t k,

@@ -29,7 +29,8 @@ ML2_MAX_TOPK = 16384
 EXPORTED = (
     "ml2_load_ensemble", "ml2_free_ensemble", "ml2_ensemble_num_features",
     "ml2_ensemble_num_trees", "ml2_ensemble_depth", "ml2_score_validity",
-    "ml2_score_perf", "ml2_topk_workspace_bytes", "ml2_filter_topk", "ml2_rerank",
+    "ml2_score_perf", "ml2_topk_workspace_bytes", "ml2_filter_topk", "ml2_filter_topk_noalloc",
+    "ml2_rerank",
     "ml2_rerank_workspace_bytes",
     "ml2_explorer_create", "ml2_explorer_free", "ml2_explorer_reset", "ml2_explorer_rounds",
     "ml2_explorer_round", "ml2_last_error",
@@ -87,6 +88,8 @@ def lib():
         L.ml2_topk_workspace_bytes.argtypes = [I64, I32, ctypes.POINTER(SZ)]
         L.ml2_filter_topk.restype = I32
         L.ml2_filter_topk.argtypes = [P, P, I64, I32, P, P, P, P, SZ, P]
+        L.ml2_filter_topk_noalloc.restype = I32
+        L.ml2_filter_topk_noalloc.argtypes = [P, P, I64, I32, P, P, P, P]
         L.ml2_rerank.restype = I32
         L.ml2_rerank.argtypes = [P, P, I64, I64, P, I32, I32, P, P, P, P, P, SZ, P]
         L.ml2_rerank_workspace_bytes.restype = I32
@@ -244,6 +247,15 @@ def ml2_filter_topk(valid, scores, k: int, topk_idx, topk_score, num_selected, w
     _check(lib().ml2_filter_topk(_ptr(valid), _ptr(scores), n, k, _ptr(topk_idx),
                                  _ptr(topk_score), _ptr(num_selected), _ptr(workspace),
                                  workspace_bytes, _stream(stream)))
+
+
+def ml2_filter_topk_noalloc(valid, scores, k: int, topk_idx, topk_score, num_selected,
+                            n: int | None = None, stream=None) -> None:
+    """ml2_filter_topk with the library's static workspace (allocates nothing)."""
+    if n is None:
+        n = scores.shape[0]
+    _check(lib().ml2_filter_topk_noalloc(_ptr(valid), _ptr(scores), n, k, _ptr(topk_idx),
+                                         _ptr(topk_score), _ptr(num_selected), _stream(stream)))
 
 
 def ml2_rerank_workspace_bytes(a: Ensemble, m: int) -> int:

@@ -241,6 +241,21 @@ def test_filter_topk_argument_errors():
     assert st == ml2.ML2_ERR_UNSUPPORTED
 
 
+def test_filter_topk_noalloc_argument_errors():
+    """The allocation-free selection validates like ml2_filter_topk (no
+    workspace argument) before touching the device."""
+    L = ml2.lib()
+    P = 1 << 20  # never dereferenced: every case fails validation first
+    for n, k, scores, idx, num in ((-1, 8, P, P, P), (100, -1, P, P, P), (100, 8, P, P, None),
+                                   (100, 8, None, P, P), (100, 8, P, None, P),
+                                   (1 << 31, 8, P, P, P)):
+        st = L.ml2_filter_topk_noalloc(None, scores, n, k, idx, P, num, None)
+        assert st == ml2.ML2_ERR_INVALID_ARG, (n, k)
+    st = L.ml2_filter_topk_noalloc(None, P, 100, ml2.ML2_MAX_TOPK + 1, P, P, P, None)
+    assert st == ml2.ML2_ERR_UNSUPPORTED
+    assert "static" in L.ml2_last_error().decode()
+
+
 def test_rerank_null_ensemble():
     L = ml2.lib()
     P = 1 << 20  # never dereferenced: the NULL ensemble fails validation first
