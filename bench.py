@@ -249,6 +249,92 @@ def explore(args, w, X, v, p, dev) -> int:
     return 0
 
 
+def explore_stream(args, w, v, p, dev) -> int:
+    """The explorer's rounds over a pool that arrives in row chunks (Section
+    2; N = 10, alpha = 1 in Section 3): each round streams every chunk of the
+    pool through ml2_stream_explorer_chunk.  Timed two ways: chunks that are
+    slices of a pool resident in HBM (the scoring rate), and chunks copied
+    from pinned host memory into two device staging buffers on a copy
+    stream, overlapped with the scoring of the previous chunk (the rate with
+    the host-to-device copies included)."""
+    import torch
+    import gen
+    from paper_2411_10764_amd import ml2
+    N = args.N
+    k = int(round((args.alpha + 1) * N))
+    rows = args.chunk_rows
+    R = args.explore_stream
+    a = ml2.ml2_load_ensemble(w.second_level()) if w.a_trees else None
+    ex = ml2.StreamExplorer(v, p, a, rows, k, N, 2 * R + 4)
+    spans = [(r0, min(rows, w.n - r0)) for r0 in range(0, w.n, rows)]
+    idx = torch.empty(N, dtype=torch.int32, device=dev)
+    top = torch.empty(N, dtype=torch.float32, device=dev)
+    num = torch.empty(1, dtype=torch.int32, device=dev)
+    main = torch.cuda.current_stream()
+
+    _log(f"pool {w.n} x {w.F} in {len(spans)} chunks of {rows} rows; pinned host copy")
+    host = torch.empty((w.n, w.F), dtype=torch.float32, pin_memory=True)
+    hn = host.numpy()
+    for r0, m in spans:
+        gen.features(w.seed, m, w.F, w.K, row0=r0, out=hn[r0:r0 + m], missing=w.missing)
+    X = torch.empty((w.n, w.F), dtype=torch.float32, device=dev)
+    X.copy_(host)
+    torch.cuda.synchronize()
+
+    def resident_round():
+        ex.begin(main)
+        for r0, m in spans:
+            ex.chunk(X[r0:r0 + m], r0, main)
+        ex.end(idx, top, num, main)
+
+    copy = torch.cuda.Stream()
+    stage = [torch.empty((rows, w.F), dtype=torch.float32, device=dev) for _ in range(2)]
+    copied = [torch.cuda.Event() for _ in range(2)]
+    used = [torch.cuda.Event() for _ in range(2)]
+    for e in used:
+        e.record(main)
+
+    def streamed_round():
+        ex.begin(main)
+        for c, (r0, m) in enumerate(spans):
+            b = c % 2
+            copy.wait_event(used[b])
+            with torch.cuda.stream(copy):
+                stage[b][:m].copy_(host[r0:r0 + m], non_blocking=True)
+            copied[b].record(copy)
+            main.wait_event(copied[b])
+            ex.chunk(stage[b][:m], r0, main)
+            used[b].record(main)
+        ex.end(idx, top, num, main)
+
+    out = {"metric": "explorer rounds/sec (pool streamed in row chunks)", "unit": "rounds/s",
+           "n_gpus": 1, "higher_is_better": True, "dtype": "f32", "data": "synthetic",
+           "config": {"workload": w.name, "candidates": w.n, "features": w.F, "N": N,
+                      "alpha": args.alpha, "held_per_round": k, "chunk_rows": rows,
+                      "chunks": len(spans), "rounds": R,
+                      "second_level": f"{w.a_trees} trees x depth {w.a_depth}" if a else None}}
+    for mode, fn in (("resident_chunks", resident_round), ("host_streamed", streamed_round)):
+        ex.reset()
+        fn()  # warm
+        torch.cuda.synchronize()
+        ex.reset()
+        t0 = time.perf_counter()
+        for _ in range(R):
+            fn()
+        torch.cuda.synchronize()
+        dt = (time.perf_counter() - t0) / R
+        out[mode] = {"rounds_per_s": 1.0 / dt, "ms_per_round": 1000.0 * dt,
+                     "candidates_per_s": w.n / dt,
+                     "proposed_last_round": int(num.item())}
+        if mode == "host_streamed":
+            out[mode]["host_to_device_gbs"] = 4.0 * w.F * w.n / dt / 1e9
+        _log(f"{mode}: {1000.0 * dt:.3f} ms per round over {R} rounds")
+    out["value"] = out["resident_chunks"]["rounds_per_s"]
+    ex.free()
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def _print(out) -> int:
     print(json.dumps(out), flush=True)
     return 0
@@ -306,6 +392,10 @@ def main() -> int:
     ap.add_argument("--explore", type=int, default=0, metavar="ROUNDS",
                     help="time ROUNDS explorer rounds (N = --N proposed per round, "
                          "(alpha+1)N held) instead of the scoring step")
+    ap.add_argument("--explore-stream", type=int, default=0, metavar="ROUNDS",
+                    help="time ROUNDS explorer rounds over the pool streamed in row chunks "
+                         "(resident slices and pinned-host copies)")
+    ap.add_argument("--chunk-rows", type=int, default=1 << 21)
     ap.add_argument("--N", type=int, default=10)
     ap.add_argument("--alpha", type=float, default=1.0)
     args = ap.parse_args()
@@ -330,6 +420,10 @@ def main() -> int:
     dev = torch.device("cuda:0")
     _log(f"workload {w.name}: n={w.n} F={w.F} V={w.v_trees}x{w.v_depth} "
          f"P={w.p_trees}x{w.p_depth} k={w.k}; generating features")
+    if args.explore_stream:
+        v = ml2.ml2_load_ensemble(w.validity())
+        p = ml2.ml2_load_ensemble(w.perf())
+        return explore_stream(args, w, v, p, dev)
     t0 = time.perf_counter()
     X = torch.empty((w.n, w.F), dtype=torch.float32, device=dev)
     chunk = 1 << 21
@@ -347,6 +441,7 @@ def main() -> int:
     p = ml2.ml2_load_ensemble(w.perf())
     if args.explore:
         return explore(args, w, X, v, p, dev)
+
     pipe = ml2.Pipeline(v, p, w.n, w.k, device=dev)
     second = w.a_trees > 0
     if second:  # model A re-ranks the k held configurations and keeps w.keep

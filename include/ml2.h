@@ -55,6 +55,7 @@ typedef enum {
 #define ML2_MAX_TREE_NODES 3062 /* nodes of one tree in the ragged layout */
 #define ML2_MAX_FEATURES 256    /* num_features of an ensemble */
 #define ML2_MAX_TOPK 16384      /* k of ml2_filter_topk; m and keep of ml2_rerank */
+#define ML2_MAX_STREAM_K 4096   /* k of ml2_stream_explorer_create */
 
 typedef struct ml2_ensemble ml2_ensemble; /* opaque; immutable after load */
 
@@ -278,6 +279,66 @@ int32_t ml2_explorer_rounds(const ml2_explorer *ex);
 ml2_status ml2_explorer_round(ml2_explorer *ex, const float *X, int64_t ld, int32_t rescore,
                               int32_t *out_idx, float *out_score, int32_t *num_selected,
                               void *stream);
+
+/*
+ * The configuration explorer over a pool that arrives in chunks of rows
+ * (Section 2, "Configuration Explorer": the explorer applies V and P to the
+ * candidate configurations until (alpha+1)*N are held, model A keeps N, and a
+ * configuration proposed once is not proposed again).  For search spaces that
+ * are generated, read or copied to the device a piece at a time instead of
+ * held in one resident matrix.  A round is
+ *   ml2_stream_explorer_begin, ml2_stream_explorer_chunk for every chunk of
+ *   the pool, ml2_stream_explorer_end;
+ * its result is the same, bit for bit, as that of a round of ml2_explorer
+ * over the pool of the distinct rows the chunks carry, in row order
+ * (a row is identified by its pool row number; the k held are the best
+ * accepted, not yet proposed rows by (P score desc, pool row asc), model A
+ * or P's order keeps `keep`).  A chunk holds pool rows row0 .. row0+m-1; chunks
+ * may come in any order, leave gaps and overlap: a row that arrives twice in
+ * a round is held once (its features must be the same in every chunk).
+ * Model A scores each chunk's selection while the chunk is on the device, so
+ * no chunk is needed after its call returns (the caller may reuse its
+ * memory once the stream has passed the call).
+ * v, p, a: ensembles as for ml2_explorer_create (a may be NULL);
+ * max_chunk_rows: the largest m of any chunk; k = (alpha+1)*N held, keep = N
+ * proposed per round, max_rounds rounds before a reset.  The explorer owns
+ * its device buffers (about 5 bytes per chunk row plus the selection's
+ * workspace); it refers to, but does not own, its ensembles.
+ * Errors: INVALID_ARG (NULL out/v/p, max_chunk_rows < 1, keep < 1 or > k,
+ * max_rounds < 1, ensembles on another device), UNSUPPORTED
+ * (k > ML2_MAX_STREAM_K), OUT_OF_MEMORY, HIP.
+ */
+typedef struct ml2_stream_explorer ml2_stream_explorer;
+ml2_status ml2_stream_explorer_create(const ml2_ensemble *v, const ml2_ensemble *p,
+                                      const ml2_ensemble *a, int64_t max_chunk_rows, int32_t k,
+                                      int32_t keep, int32_t max_rounds,
+                                      ml2_stream_explorer **out);
+/* Releases the explorer's memory (NULL is a no-op); the caller must have
+ * finished every call enqueued on it. */
+void ml2_stream_explorer_free(ml2_stream_explorer *ex);
+/* Forgets every proposed row and any open round (INVALID_ARG if NULL). */
+ml2_status ml2_stream_explorer_reset(ml2_stream_explorer *ex);
+/* Rounds ended since creation or the last reset (-1 for NULL). */
+int32_t ml2_stream_explorer_rounds(const ml2_stream_explorer *ex);
+/* Opens a round: nothing is held (enqueued on `stream`).  INVALID_ARG if a
+ * round is open or every round is used, or on another device; HIP. */
+ml2_status ml2_stream_explorer_begin(ml2_stream_explorer *ex, void *stream);
+/* Scores chunk X (float32 [m][ld] device, ld >= every ensemble's feature
+ * count, 4-byte aligned; pool rows row0 .. row0+m-1) and updates the held
+ * set: its accepted rows not proposed in earlier rounds compete with those
+ * held.  m = 0 does nothing.  All of it is enqueued on `stream`; calls on one
+ * explorer must be ordered on one stream.  INVALID_ARG (no open round, m < 0
+ * or > max_chunk_rows, row0 < 0 or row0 + m > 2^31 - 1, NULL X with m > 0,
+ * ld too small, misaligned X), UNSUPPORTED, HIP. */
+ml2_status ml2_stream_explorer_chunk(ml2_stream_explorer *ex, const float *X, int64_t m,
+                                     int64_t ld, int64_t row0, void *stream);
+/* Closes the round: writes the keep rows proposed (out_idx int32 [keep],
+ * pool rows; out_score float32 [keep], model A's scores, or P's without A,
+ * bit for bit; -1 / -inf padding once the pool runs dry; *num_selected, all
+ * device) and records them as proposed.  INVALID_ARG (NULL outputs, no open
+ * round), HIP. */
+ml2_status ml2_stream_explorer_end(ml2_stream_explorer *ex, int32_t *out_idx, float *out_score,
+                                   int32_t *num_selected, void *stream);
 
 /* Thread-local description of the last non-OK status on this thread. */
 const char *ml2_last_error(void);

@@ -222,6 +222,38 @@ def explore(v_ens, p_ens, a_ens, X, k: int, keep: int, rounds: int, threads: int
     return out
 
 
+def explore_stream(v_ens, p_ens, a_ens, chunks, k: int, keep: int, rounds: int,
+                   threads: int = 1):
+    """The explorer's rounds over a pool that arrives in row chunks
+    (Section 2: the explorer applies V and P to the candidate configurations
+    until (alpha+1)N are held and model A keeps N; a configuration proposed
+    once is not proposed again).  ``chunks`` is the list of (row0, X_chunk)
+    the pool arrives in, the same every round: row ``row0 + i`` of the pool
+    is ``X_chunk[i]``; a row that arrives in several chunks is one
+    configuration.  By definition a round works on the set of distinct rows,
+    so this runs ``explore`` over those rows in row order (ties by position
+    are then ties by row) and reports pool rows.  Returns [(idx i32 [keep],
+    score f32 [keep], num)] per round; -1/-inf pad a round once the pool runs
+    dry."""
+    rows = {}
+    F = None
+    for row0, Xc in chunks:
+        Xc = np.asarray(Xc, np.float32)
+        F = Xc.shape[1] if Xc.ndim == 2 else F
+        for i in range(Xc.shape[0]):
+            rows.setdefault(int(row0) + i, Xc[i])
+    ids = np.array(sorted(rows), np.int64)
+    if ids.size == 0:
+        return [(np.full(keep, -1, np.int32), np.full(keep, -np.inf, np.float32), 0)
+                for _ in range(rounds)]
+    X = np.stack([rows[int(i)] for i in ids]).astype(np.float32)
+    out = []
+    for idx, top, num in explore(v_ens, p_ens, a_ens, X, k, keep, rounds, threads):
+        pool = np.where(idx >= 0, ids[np.maximum(idx, 0)], -1).astype(np.int32)
+        out.append((pool, top, num))
+    return out
+
+
 def pipeline(v_ens, p_ens, X, k: int, threads: int = 1):
     """Validity -> masked performance -> top-k, as the explorer applies them."""
     valid, marg = validity(v_ens, X, threads)

@@ -41,6 +41,30 @@ struct ml2_explorer {
   void *a_ws;         // second-level leaves
 };
 
+// Device state of a streamed explorer (see ml2_stream_explorer_create).
+struct ml2_stream_explorer {
+  const ml2_ensemble *v, *p, *a;  // not owned
+  int device;
+  int64_t max_rows;   // rows of the largest chunk
+  int32_t k, keep, max_rounds, rounds;
+  bool open;          // a round has begun and not ended
+  int cur;            // which held set is current (0 or 1)
+  void *block;        // one allocation holding every buffer below
+  uint8_t *valid;     // [max_rows] chunk mask
+  float *score;       // [max_rows] chunk P scores
+  int32_t *tk_idx;    // [k] chunk selection (chunk-local rows)
+  float *tk_score;
+  int32_t *tk_num;
+  float *a_scores;    // [k] model A's scores of the chunk selection
+  int32_t *held_id[2];
+  float *held_p[2], *held_a[2];
+  int32_t *held_n[2];
+  int32_t *proposed;  // [max_rounds * keep] pool rows proposed so far (-1 padding)
+  void *ws;           // top-k workspace
+  size_t ws_bytes;
+  void *a_ws;         // second-level leaves
+};
+
 namespace {
 
 thread_local std::string g_last_error;
@@ -780,6 +804,204 @@ ml2_status ml2_explorer_round(ml2_explorer *ex, const float *X, int64_t ld, int3
   if (e != hipSuccess) return hip_fail(e, "explorer selection launch");
   ex->rounds += 1;
   ex->scored = true;
+  return ML2_OK;
+}
+
+// ---- the explorer over a streamed pool -------------------------------------------
+
+ml2_status ml2_stream_explorer_create(const ml2_ensemble *v, const ml2_ensemble *p,
+                                      const ml2_ensemble *a, int64_t max_chunk_rows, int32_t k,
+                                      int32_t keep, int32_t max_rounds,
+                                      ml2_stream_explorer **out) {
+  if (!out) return fail(ML2_ERR_INVALID_ARG, "ml2_stream_explorer_create: out is NULL");
+  *out = nullptr;
+  if (!v || !p)
+    return fail(ML2_ERR_INVALID_ARG, "ml2_stream_explorer_create: NULL V or P ensemble");
+  if (max_chunk_rows < 1 || max_chunk_rows > (int64_t)INT32_MAX)
+    return fail(ML2_ERR_INVALID_ARG,
+                "ml2_stream_explorer_create: max_chunk_rows = %lld outside [1, 2^31-1]",
+                (long long)max_chunk_rows);
+  if (k < 1 || keep < 1 || keep > k || max_rounds < 1)
+    return fail(ML2_ERR_INVALID_ARG,
+                "ml2_stream_explorer_create: need 1 <= keep <= k and max_rounds >= 1 (k = %d, "
+                "keep = %d, max_rounds = %d)", k, keep, max_rounds);
+  if (k > ML2_MAX_STREAM_K)
+    return fail(ML2_ERR_UNSUPPORTED, "ml2_stream_explorer_create: k = %d > %d", k,
+                ML2_MAX_STREAM_K);
+  if ((int64_t)max_rounds * keep > (int64_t)INT32_MAX)
+    return fail(ML2_ERR_INVALID_ARG, "ml2_stream_explorer_create: max_rounds * keep overflows");
+  int dev = 0;
+  ml2_status st = current_device(&dev);
+  if (st != ML2_OK) return st;
+  if (v->f.device != dev || p->f.device != dev || (a && a->f.device != dev))
+    return fail(ML2_ERR_INVALID_ARG, "ml2_stream_explorer_create: ensembles not on device %d",
+                dev);
+  auto up = [](size_t b) { return (b + 255) & ~(size_t)255; };
+  const size_t n = (size_t)max_chunk_rows, kk = (size_t)k;
+  const size_t ws = ml2::topk_workspace_bytes(max_chunk_rows, k);
+  const size_t a_ws = a ? ml2::rows_workspace_bytes(a->f, k) : 0;
+  const size_t sizes[] = {up(n), up(4 * n), up(4 * kk), up(4 * kk), up(4), up(4 * kk),
+                          up(4 * kk), up(4 * kk), up(4 * kk), up(4),
+                          up(4 * kk), up(4 * kk), up(4 * kk), up(4),
+                          up(4 * (size_t)max_rounds * keep), up(ws), up(a_ws)};
+  size_t total = 0;
+  for (size_t b : sizes) total += b;
+  ml2_stream_explorer *ex = new (std::nothrow) ml2_stream_explorer{};
+  if (!ex)
+    return fail(ML2_ERR_OUT_OF_MEMORY, "ml2_stream_explorer_create: handle allocation failed");
+  hipError_t e = hipMalloc(&ex->block, total);
+  if (e != hipSuccess) {
+    delete ex;
+    if (e == hipErrorOutOfMemory)
+      return fail(ML2_ERR_OUT_OF_MEMORY, "ml2_stream_explorer_create: hipMalloc(%zu)", total);
+    return hip_fail(e, "ml2_stream_explorer_create: hipMalloc");
+  }
+  char *c = static_cast<char *>(ex->block);
+  size_t i = 0;
+  auto take = [&](size_t) {
+    char *q = c;
+    c += sizes[i++];
+    return q;
+  };
+  ex->valid = reinterpret_cast<uint8_t *>(take(0));
+  ex->score = reinterpret_cast<float *>(take(0));
+  ex->tk_idx = reinterpret_cast<int32_t *>(take(0));
+  ex->tk_score = reinterpret_cast<float *>(take(0));
+  ex->tk_num = reinterpret_cast<int32_t *>(take(0));
+  ex->a_scores = reinterpret_cast<float *>(take(0));
+  for (int h = 0; h < 2; ++h) {
+    ex->held_id[h] = reinterpret_cast<int32_t *>(take(0));
+    ex->held_p[h] = reinterpret_cast<float *>(take(0));
+    ex->held_a[h] = reinterpret_cast<float *>(take(0));
+    ex->held_n[h] = reinterpret_cast<int32_t *>(take(0));
+  }
+  ex->proposed = reinterpret_cast<int32_t *>(take(0));
+  ex->ws_bytes = sizes[i];
+  ex->ws = take(0);
+  ex->a_ws = take(0);
+  ex->v = v;
+  ex->p = p;
+  ex->a = a;
+  ex->device = dev;
+  ex->max_rows = max_chunk_rows;
+  ex->k = k;
+  ex->keep = keep;
+  ex->max_rounds = max_rounds;
+  *out = ex;
+  return ML2_OK;
+}
+
+void ml2_stream_explorer_free(ml2_stream_explorer *ex) {
+  if (!ex) return;
+  int cur = 0;
+  const bool other = hipGetDevice(&cur) == hipSuccess && cur != ex->device;
+  if (other) (void)hipSetDevice(ex->device);
+  (void)hipFree(ex->block);
+  if (other) (void)hipSetDevice(cur);
+  delete ex;
+}
+
+ml2_status ml2_stream_explorer_reset(ml2_stream_explorer *ex) {
+  if (!ex) return fail(ML2_ERR_INVALID_ARG, "ml2_stream_explorer_reset: explorer is NULL");
+  ex->rounds = 0;
+  ex->open = false;
+  return ML2_OK;
+}
+
+int32_t ml2_stream_explorer_rounds(const ml2_stream_explorer *ex) {
+  return ex ? ex->rounds : -1;
+}
+
+ml2_status ml2_stream_explorer_begin(ml2_stream_explorer *ex, void *stream) {
+  if (!ex) return fail(ML2_ERR_INVALID_ARG, "ml2_stream_explorer_begin: explorer is NULL");
+  if (ex->open)
+    return fail(ML2_ERR_INVALID_ARG, "ml2_stream_explorer_begin: the round has begun already");
+  if (ex->rounds >= ex->max_rounds)
+    return fail(ML2_ERR_INVALID_ARG, "ml2_stream_explorer_begin: all %d rounds used (reset first)",
+                ex->max_rounds);
+  int dev = 0;
+  ml2_status st = current_device(&dev);
+  if (st != ML2_OK) return st;
+  if (dev != ex->device)
+    return fail(ML2_ERR_INVALID_ARG, "ml2_stream_explorer_begin: explorer lives on device %d",
+                ex->device);
+  const int h = ex->cur;
+  hipError_t e = ml2::launch_held_reset(ex->held_id[h], ex->held_p[h], ex->held_a[h],
+                                        ex->held_n[h], ex->k, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "ml2_stream_explorer_begin: launch");
+  ex->open = true;
+  return ML2_OK;
+}
+
+ml2_status ml2_stream_explorer_chunk(ml2_stream_explorer *ex, const float *X, int64_t m,
+                                     int64_t ld, int64_t row0, void *stream) {
+  if (!ex) return fail(ML2_ERR_INVALID_ARG, "ml2_stream_explorer_chunk: explorer is NULL");
+  if (!ex->open)
+    return fail(ML2_ERR_INVALID_ARG, "ml2_stream_explorer_chunk: no round has begun");
+  if (m < 0 || m > ex->max_rows)
+    return fail(ML2_ERR_INVALID_ARG, "ml2_stream_explorer_chunk: m = %lld outside [0, %lld]",
+                (long long)m, (long long)ex->max_rows);
+  if (row0 < 0 || row0 + m > (int64_t)INT32_MAX)
+    return fail(ML2_ERR_INVALID_ARG,
+                "ml2_stream_explorer_chunk: rows [%lld, %lld) outside [0, 2^31-1)",
+                (long long)row0, (long long)(row0 + m));
+  int dev = 0;
+  const ml2_ensemble *models[3] = {ex->v, ex->p, ex->a};
+  for (const ml2_ensemble *e : models) {
+    if (!e) continue;
+    ml2_status st = check_stream_args(e, X, m, ld, X, "ml2_stream_explorer_chunk", &dev);
+    if (st != ML2_OK) return st;
+  }
+  if (m == 0) return ML2_OK;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const int cus = cu_count(dev);
+  ml2::WalkPlan pv, pp;
+  const char *why = nullptr;
+  if (!ml2::plan_walk(ex->v->f, m, cus, &pv, &why) || !ml2::plan_walk(ex->p->f, m, cus, &pp, &why))
+    return fail(ML2_ERR_UNSUPPORTED, "ml2_stream_explorer_chunk: %s", why);
+  const int h = ex->cur;
+  hipError_t e = ml2::launch_validity(ex->v->f, pv, X, m, ld, ex->valid, nullptr, s);
+  if (e == hipSuccess)
+    e = ml2::launch_exclude_range(ex->valid, row0, m, ex->proposed, ex->rounds * ex->keep, s);
+  if (e == hipSuccess) e = ml2::launch_perf(ex->p->f, pp, X, m, ld, ex->valid, ex->score, s);
+  if (e == hipSuccess)
+    e = ml2::launch_topk(ex->valid, ex->score, m, ex->k, ex->tk_idx, ex->tk_score, ex->tk_num,
+                         ex->ws, cus, s);
+  if (e == hipSuccess && ex->a)
+    e = ml2::launch_rows(ex->a->f, X, m, ld, ex->tk_idx, ex->k, ex->a_scores, ex->a_ws, cus, s);
+  if (e == hipSuccess)
+    e = ml2::launch_merge_held(ex->held_id[h], ex->held_p[h], ex->held_a[h], ex->held_n[h],
+                               ex->tk_idx, ex->tk_score, ex->a ? ex->a_scores : nullptr,
+                               ex->tk_num, row0, ex->k, ex->held_id[1 - h], ex->held_p[1 - h],
+                               ex->held_a[1 - h], ex->held_n[1 - h], s);
+  if (e != hipSuccess) return hip_fail(e, "ml2_stream_explorer_chunk: launch");
+  ex->cur = 1 - h;
+  return ML2_OK;
+}
+
+ml2_status ml2_stream_explorer_end(ml2_stream_explorer *ex, int32_t *out_idx, float *out_score,
+                                   int32_t *num_selected, void *stream) {
+  if (!ex) return fail(ML2_ERR_INVALID_ARG, "ml2_stream_explorer_end: explorer is NULL");
+  if (!out_idx || !out_score || !num_selected)
+    return fail(ML2_ERR_INVALID_ARG, "ml2_stream_explorer_end: NULL output array");
+  if (!ex->open) return fail(ML2_ERR_INVALID_ARG, "ml2_stream_explorer_end: no round has begun");
+  int dev = 0;
+  ml2_status st = current_device(&dev);
+  if (st != ML2_OK) return st;
+  if (dev != ex->device)
+    return fail(ML2_ERR_INVALID_ARG, "ml2_stream_explorer_end: explorer lives on device %d",
+                ex->device);
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const int h = ex->cur;
+  // held rows past the held count carry row -1 and are skipped
+  hipError_t e = ml2::launch_rerank_select(ex->held_id[h], ex->held_a[h], ex->k, INT32_MAX,
+                                           ex->keep, out_idx, out_score, num_selected, s);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(ex->proposed + (size_t)ex->rounds * ex->keep, out_idx,
+                       sizeof(int32_t) * ex->keep, hipMemcpyDeviceToDevice, s);
+  if (e != hipSuccess) return hip_fail(e, "ml2_stream_explorer_end: launch");
+  ex->rounds += 1;
+  ex->open = false;
   return ML2_OK;
 }
 

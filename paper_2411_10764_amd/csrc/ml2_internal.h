@@ -121,6 +121,20 @@ hipError_t launch_topk(const uint8_t *valid, const float *scores, int64_t n, int
 hipError_t launch_exclude(uint8_t *mask, int64_t n, const int32_t *rows, int32_t m,
                           hipStream_t s);
 
+// Streamed explorer: proposed rows leave a chunk's mask (rows row0 ..
+// row0+m-1); the held count is reset; the held set absorbs a chunk's
+// selection (k best by (P desc, row asc), each row once; merge_held_lds(k)
+// bytes of LDS, k <= 4096).
+hipError_t launch_exclude_range(uint8_t *mask, int64_t row0, int64_t m, const int32_t *rows,
+                                int32_t count, hipStream_t s);
+hipError_t launch_held_reset(int32_t *held_id, float *held_p, float *held_a, int32_t *held_n,
+                             int32_t k, hipStream_t s);
+size_t merge_held_lds(int32_t k);
+hipError_t launch_merge_held(const int32_t *h_id, const float *h_p, const float *h_a,
+                             const int32_t *h_n, const int32_t *c_idx, const float *c_p,
+                             const float *c_a, const int32_t *c_n, int64_t row0, int32_t k,
+                             int32_t *o_id, float *o_p, float *o_a, int32_t *o_n, hipStream_t s);
+
 // The `keep` best of m listed rows by (score desc, pool row asc); m <= ML2_MAX_TOPK.
 hipError_t launch_rerank_select(const int32_t *rows, const float *scores, int32_t m, int64_t n,
                                 int32_t keep, int32_t *idx, float *score, int32_t *num,

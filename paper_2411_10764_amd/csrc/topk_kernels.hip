@@ -326,6 +326,135 @@ __global__ void __launch_bounds__(256) exclude_rows(uint8_t *mask, int64_t n,
   if (r >= 0 && r < n) mask[r] = 0;
 }
 
+// A chunk of pool rows row0 .. row0+m-1 (streamed explorer): rows proposed in
+// earlier rounds leave the chunk's mask, mask[r - row0] = 0 for every listed
+// row r inside the chunk (the -1 padding of short rounds never is).
+__global__ void __launch_bounds__(256) exclude_range(uint8_t *mask, int64_t row0, int64_t m,
+                                                     const int32_t *rows, int32_t count) {
+  const int32_t j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= count) return;
+  const int64_t r = rows[j];
+  if (r >= row0 && r < row0 + m) mask[r - row0] = 0;
+}
+
+// An empty held set: no rows, every slot -1 / -inf.
+__global__ void __launch_bounds__(256) held_reset(int32_t *held_id, float *held_p,
+                                                  float *held_a, int32_t *held_n, int32_t k) {
+  for (int32_t j = blockIdx.x * blockDim.x + threadIdx.x; j < k; j += gridDim.x * blockDim.x) {
+    held_id[j] = -1;
+    held_p[j] = -INFINITY;
+    held_a[j] = -INFINITY;
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) *held_n = 0;
+}
+
+// The held set of the streamed explorer after one more chunk: the k best of
+// the rows held so far (h_*, *h_n of them) and the chunk's selection (c_*,
+// *c_n of them, chunk-local indices; pool row = row0 + index) by (P score
+// desc, pool row asc), a row present in both counted once.  Each entry
+// carries its P score and its second-level score (model A's, or P's again
+// when c_a is NULL), copied bit for bit.  One workgroup: keys
+// (ord(P) << 32) | (0xFFFFFFFF - row) and their source positions are sorted
+// together in LDS (bitonic, descending); equal keys are the same row with the
+// same score, so every key after an equal one is dropped.
+__global__ void __launch_bounds__(kSortThreads) merge_held(
+    const int32_t *h_id, const float *h_p, const float *h_a, const int32_t *h_n,
+    const int32_t *c_idx, const float *c_p, const float *c_a, const int32_t *c_n, int64_t row0,
+    int32_t k, int32_t *o_id, float *o_p, float *o_a, int32_t *o_n) {
+  extern __shared__ unsigned long long keys[];
+  __shared__ int warp_sum[kSortThreads / 64 + 1];
+  int size = 1;
+  while (size < 2 * k) size <<= 1;
+  int32_t *pos = reinterpret_cast<int32_t *>(keys + size);
+  const int hn = min(*h_n, k), cn = min(*c_n, k);
+  for (int j = threadIdx.x; j < size; j += blockDim.x) {
+    unsigned long long key = 0ull;
+    if (j < hn) {
+      key = make_key(h_p[j], h_id[j]);
+    } else if (j >= k && j - k < cn) {
+      key = make_key(c_p[j - k], row0 + c_idx[j - k]);
+    }
+    keys[j] = key;
+    pos[j] = j;
+  }
+  __syncthreads();
+  for (int len = 2; len <= size; len <<= 1) {
+    for (int stride = len >> 1; stride > 0; stride >>= 1) {
+      for (int j = threadIdx.x; j < size; j += blockDim.x) {
+        const int p = j ^ stride;
+        if (p > j) {
+          const unsigned long long a = keys[j], b = keys[p];
+          const bool desc = (j & len) == 0;
+          if (desc ? (a < b) : (a > b)) {
+            keys[j] = b;
+            keys[p] = a;
+            const int32_t t = pos[j];
+            pos[j] = pos[p];
+            pos[p] = t;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  // Rank of each first occurrence: each thread owns a run of consecutive
+  // sorted entries; the runs' counts are scanned across the workgroup.
+  const int per = size / blockDim.x > 0 ? size / blockDim.x : 1;
+  const int lo = threadIdx.x * per;
+  const bool owner = lo < size;
+  int mine = 0;
+  if (owner)
+    for (int j = lo; j < lo + per; ++j)
+      mine += (keys[j] != 0ull && (j == 0 || keys[j] != keys[j - 1])) ? 1 : 0;
+  // inclusive scan of `mine` over the threads: waves, then wave totals
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int incl = mine;
+  for (int d = 1; d < 64; d <<= 1) {
+    const int v = __shfl_up(incl, d);
+    if (lane >= d) incl += v;
+  }
+  if (lane == 63) warp_sum[wave] = incl;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int acc = 0;
+    for (int w = 0; w < (int)(blockDim.x >> 6); ++w) {
+      const int t = warp_sum[w];
+      warp_sum[w] = acc;
+      acc += t;
+    }
+    warp_sum[blockDim.x >> 6] = acc;
+  }
+  __syncthreads();
+  const int unique = warp_sum[blockDim.x >> 6];
+  if (owner) {
+    int r = warp_sum[wave] + incl - mine;  // rank of this run's first occurrence
+    for (int j = lo; j < lo + per; ++j) {
+      if (keys[j] == 0ull || (j > 0 && keys[j] == keys[j - 1])) continue;
+      if (r < k) {
+        const int src = pos[j];
+        if (src < k) {
+          o_id[r] = h_id[src];
+          o_p[r] = h_p[src];
+          o_a[r] = h_a[src];
+        } else {
+          const int c = src - k;
+          o_id[r] = (int32_t)(row0 + c_idx[c]);
+          o_p[r] = c_p[c];
+          o_a[r] = c_a ? c_a[c] : c_p[c];
+        }
+      }
+      ++r;
+    }
+  }
+  const int held = min(unique, k);
+  for (int r = held + threadIdx.x; r < k; r += blockDim.x) {
+    o_id[r] = -1;
+    o_p[r] = -INFINITY;
+    o_a[r] = -INFINITY;
+  }
+  if (threadIdx.x == 0) *o_n = held;
+}
+
 }  // namespace
 
 size_t topk_workspace_bytes(int64_t n, int32_t k) {
@@ -418,6 +547,40 @@ hipError_t launch_exclude(uint8_t *mask, int64_t n, const int32_t *rows, int32_t
   if (m <= 0) return hipSuccess;
   hipLaunchKernelGGL(exclude_rows, dim3((unsigned)((m + 255) / 256)), dim3(256), 0, s, mask, n,
                      rows, m);
+  return hipGetLastError();
+}
+
+hipError_t launch_exclude_range(uint8_t *mask, int64_t row0, int64_t m, const int32_t *rows,
+                                int32_t count, hipStream_t s) {
+  if (count <= 0 || m <= 0) return hipSuccess;
+  hipLaunchKernelGGL(exclude_range, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, s, mask,
+                     row0, m, rows, count);
+  return hipGetLastError();
+}
+
+hipError_t launch_held_reset(int32_t *held_id, float *held_p, float *held_a, int32_t *held_n,
+                             int32_t k, hipStream_t s) {
+  hipLaunchKernelGGL(held_reset, dim3((unsigned)((k + 255) / 256)), dim3(256), 0, s, held_id,
+                     held_p, held_a, held_n, k);
+  return hipGetLastError();
+}
+
+size_t merge_held_lds(int32_t k) {
+  int size = 1;
+  while (size < 2 * k) size <<= 1;
+  return (size_t)size * (sizeof(unsigned long long) + sizeof(int32_t));
+}
+
+hipError_t launch_merge_held(const int32_t *h_id, const float *h_p, const float *h_a,
+                             const int32_t *h_n, const int32_t *c_idx, const float *c_p,
+                             const float *c_a, const int32_t *c_n, int64_t row0, int32_t k,
+                             int32_t *o_id, float *o_p, float *o_a, int32_t *o_n, hipStream_t s) {
+  const size_t lds = merge_held_lds(k);
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&merge_held),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(merge_held, dim3(1), dim3(kSortThreads), lds, s, h_id, h_p, h_a, h_n, c_idx,
+                     c_p, c_a, c_n, row0, k, o_id, o_p, o_a, o_n);
   return hipGetLastError();
 }
 

@@ -25,6 +25,7 @@ ML2_MAX_DEPTH = 32
 ML2_MAX_TREE_NODES = 3062
 ML2_MAX_FEATURES = 256
 ML2_MAX_TOPK = 16384
+ML2_MAX_STREAM_K = 4096
 
 EXPORTED = (
     "ml2_load_ensemble", "ml2_free_ensemble", "ml2_ensemble_num_features",
@@ -33,7 +34,9 @@ EXPORTED = (
     "ml2_rerank",
     "ml2_rerank_workspace_bytes",
     "ml2_explorer_create", "ml2_explorer_free", "ml2_explorer_reset", "ml2_explorer_rounds",
-    "ml2_explorer_round", "ml2_last_error",
+    "ml2_explorer_round", "ml2_stream_explorer_create", "ml2_stream_explorer_free",
+    "ml2_stream_explorer_reset", "ml2_stream_explorer_rounds", "ml2_stream_explorer_begin",
+    "ml2_stream_explorer_chunk", "ml2_stream_explorer_end", "ml2_last_error",
 )
 # include/ml2_probe.h: microbenchmarks behind the roofline figures
 EXPORTED_PROBE = ("ml2_probe_visit", "ml2_probe_lds", "ml2_probe_valu", "ml2_tune_walk_plan",
@@ -104,6 +107,20 @@ def lib():
         L.ml2_explorer_rounds.argtypes = [P]
         L.ml2_explorer_round.restype = I32
         L.ml2_explorer_round.argtypes = [P, P, I64, I32, P, P, P, P]
+        L.ml2_stream_explorer_create.restype = I32
+        L.ml2_stream_explorer_create.argtypes = [P, P, P, I64, I32, I32, I32, ctypes.POINTER(P)]
+        L.ml2_stream_explorer_free.restype = None
+        L.ml2_stream_explorer_free.argtypes = [P]
+        L.ml2_stream_explorer_reset.restype = I32
+        L.ml2_stream_explorer_reset.argtypes = [P]
+        L.ml2_stream_explorer_rounds.restype = I32
+        L.ml2_stream_explorer_rounds.argtypes = [P]
+        L.ml2_stream_explorer_begin.restype = I32
+        L.ml2_stream_explorer_begin.argtypes = [P, P]
+        L.ml2_stream_explorer_chunk.restype = I32
+        L.ml2_stream_explorer_chunk.argtypes = [P, P, I64, I64, I64, P]
+        L.ml2_stream_explorer_end.restype = I32
+        L.ml2_stream_explorer_end.argtypes = [P, P, P, P, P]
         L.ml2_last_error.restype = ctypes.c_char_p
         L.ml2_last_error.argtypes = []
         D = ctypes.POINTER(ctypes.c_double)
@@ -308,6 +325,50 @@ class Explorer:
     def free(self) -> None:
         if self.handle:
             lib().ml2_explorer_free(self.handle)
+            self.handle = None
+
+    def __del__(self):  # pragma: no cover - interpreter shutdown order
+        try:
+            self.free()
+        except Exception:
+            pass
+
+
+class StreamExplorer:
+    """An ml2_stream_explorer: the explorer's rounds over a pool that arrives
+    in chunks of rows (owns the handle; holds references to its ensembles)."""
+
+    def __init__(self, v: Ensemble, p: Ensemble, a: Ensemble | None, max_chunk_rows: int,
+                 k: int, keep: int, max_rounds: int):
+        h = ctypes.c_void_p()
+        _check(lib().ml2_stream_explorer_create(v.handle, p.handle, a.handle if a else None,
+                                                max_chunk_rows, k, keep, max_rounds,
+                                                ctypes.byref(h)))
+        self.handle = h.value
+        self.models = (v, p, a)
+        self.k, self.keep = k, keep
+
+    @property
+    def rounds(self) -> int:
+        return lib().ml2_stream_explorer_rounds(self.handle)
+
+    def reset(self) -> None:
+        _check(lib().ml2_stream_explorer_reset(self.handle))
+
+    def begin(self, stream=None) -> None:
+        _check(lib().ml2_stream_explorer_begin(self.handle, _stream(stream)))
+
+    def chunk(self, X, row0: int, stream=None) -> None:
+        xp, m, ld = _rows(X)
+        _check(lib().ml2_stream_explorer_chunk(self.handle, xp, m, ld, row0, _stream(stream)))
+
+    def end(self, out_idx, out_score, num_selected, stream=None) -> None:
+        _check(lib().ml2_stream_explorer_end(self.handle, _ptr(out_idx), _ptr(out_score),
+                                             _ptr(num_selected), _stream(stream)))
+
+    def free(self) -> None:
+        if self.handle:
+            lib().ml2_stream_explorer_free(self.handle)
             self.handle = None
 
     def __del__(self):  # pragma: no cover - interpreter shutdown order

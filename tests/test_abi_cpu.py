@@ -82,7 +82,8 @@ def test_tune_layout_argument_errors():
 
 def test_header_constants_match_binding():
     text = open(HEADER).read()
-    for name in ("ML2_MAX_DEPTH", "ML2_MAX_TREE_NODES", "ML2_MAX_FEATURES", "ML2_MAX_TOPK"):
+    for name in ("ML2_MAX_DEPTH", "ML2_MAX_TREE_NODES", "ML2_MAX_FEATURES", "ML2_MAX_TOPK",
+                 "ML2_MAX_STREAM_K"):
         m = re.search(rf"#define {name} (\d+)", text)
         assert m and int(m.group(1)) == getattr(ml2, name)
     for name, val in (("ML2_OK", 0), ("ML2_ERR_INVALID_ARG", 1), ("ML2_ERR_UNSUPPORTED", 2),
@@ -280,3 +281,21 @@ def test_explorer_null_handles():
     assert L.ml2_explorer_reset(None) == ml2.ML2_ERR_INVALID_ARG
     assert L.ml2_explorer_rounds(None) == -1
     L.ml2_explorer_free(None)
+
+
+def test_stream_explorer_null_handles():
+    import ctypes
+    L = ml2.lib()
+    h = ctypes.c_void_p()
+    assert L.ml2_stream_explorer_create(None, None, None, 100, 4, 2, 3, ctypes.byref(h)) == \
+        ml2.ML2_ERR_INVALID_ARG
+    assert h.value is None
+    assert L.ml2_stream_explorer_create(None, None, None, 100, 4, 2, 3, None) == \
+        ml2.ML2_ERR_INVALID_ARG
+    P = 1 << 20  # never dereferenced
+    assert L.ml2_stream_explorer_begin(None, None) == ml2.ML2_ERR_INVALID_ARG
+    assert L.ml2_stream_explorer_chunk(None, P, 10, 8, 0, None) == ml2.ML2_ERR_INVALID_ARG
+    assert L.ml2_stream_explorer_end(None, P, P, P, None) == ml2.ML2_ERR_INVALID_ARG
+    assert L.ml2_stream_explorer_reset(None) == ml2.ML2_ERR_INVALID_ARG
+    assert L.ml2_stream_explorer_rounds(None) == -1
+    L.ml2_stream_explorer_free(None)
