@@ -180,7 +180,7 @@ ml2_status ml2_filter_topk(const uint8_t *valid, const float *scores, int64_t n,
  * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
  * the same selection and outputs as ml2_filter_topk, with the workspace
  * taken from a static array in the library's device code instead of an
- * argument.  The array (147,712 bytes, the workspace of k = ML2_MAX_TOPK) is
+ * argument.  The array (246,016 bytes, the workspace of k = ML2_MAX_TOPK) is
  * held by each device the library runs on until the process ends; its
  * device address is looked up on the first call on a device.  This call
  * allocates nothing.
