@@ -340,10 +340,41 @@ def _print(out) -> int:
     return 0
 
 
-def out_hbm(w, args, value, ms_per_step, t_val, t_perf, t_topk, n_valid, alg_bytes):
+def out_hbm(w, args, value, ms_per_step, t_val, t_perf, t_topk, n_valid, alg_bytes, fused):
     """The HBM-bound diagnostic: small ensembles, so reading the pool bounds
-    the step.  The roofline object covers the validity launch, which reads
-    every row once (4F bytes) and writes the mask (1 byte)."""
+    the step.  The roofline object covers the launch that reads every row
+    once (4F bytes): with one pass the fused walk, which also writes the mask
+    (1 byte) and the score (4 bytes); otherwise the validity walk (mask
+    only), with the perf walk's re-read of the accepted rows beside it."""
+    if fused:
+        f_bytes = (4.0 * w.F + 1.0 + 4.0) * w.n
+        achieved = f_bytes / (t_val / 1000.0) / 1e9
+        step_gbs = alg_bytes / (ms_per_step / 1000.0) / 1e9
+        return {
+            "metric": METRIC, "value": value, "unit": "candidates/s", "n_gpus": 1,
+            "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
+            "timing": "median of per-step HIP-event durations on the launch stream",
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+            "data": "synthetic (seeded knob + lognormal features, random perfect trees)",
+            "config": {"workload": w.name, "diagnostic": "HBM-bound: not a benchmark configuration",
+                       "candidates": w.n, "features": w.F,
+                       "validity": f"{w.v_trees} trees x depth {w.v_depth}",
+                       "perf": f"{w.p_trees} trees x depth {w.p_depth}", "k": w.k, "seed": w.seed,
+                       "invalid_fraction": 1 - n_valid / w.n, "one_pass": True},
+            "roofline": {
+                "bound": "hbm", "kernel": "fused_kernel (V then P on every row, one pass)",
+                "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                "work_per_launch": f"{f_bytes:.4g} bytes ({w.n} rows x {4 * w.F} B + mask + "
+                                   "score)",
+                "launch_ms": t_val,
+                "step": {"algorithmic_bytes": alg_bytes, "achieved_gbs": step_gbs,
+                         "frac": step_gbs / HBM_PEAK_GBS},
+            },
+            "hbm_frac": step_gbs / HBM_PEAK_GBS,
+            "kernel_ms": {"validity_perf_one_pass": t_val, "topk": t_topk},
+            "cpu_baseline": None,
+        }
     val_bytes = (4.0 * w.F + 1.0) * w.n
     perf_bytes = 4.0 * w.F * n_valid + 1.0 * w.n + 4.0 * w.n  # accepted rows, mask, scores
     achieved = val_bytes / (t_val / 1000.0) / 1e9
@@ -453,14 +484,22 @@ def main() -> int:
         a_wsb = ml2.ml2_rerank_workspace_bytes(a, w.k)
         a_ws = torch.empty(a_wsb, dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
+    # where both ensembles fit on chip together, ml2_score reads every row
+    # once and walks V and P on it (one kernel); otherwise two walks
+    fused = ml2.ml2_score_single_pass(v, p, X)
 
     def step(e=None):
         if e is not None:
             e[0].record(stream)
-        ml2.ml2_score_validity(v, X, pipe.valid, None, stream)
-        if e is not None:
-            e[1].record(stream)
-        ml2.ml2_score_perf(p, X, pipe.valid, pipe.score, stream)
+        if fused:
+            ml2.ml2_score(v, p, X, pipe.valid, None, pipe.score, stream)
+            if e is not None:
+                e[1].record(stream)
+        else:
+            ml2.ml2_score_validity(v, X, pipe.valid, None, stream)
+            if e is not None:
+                e[1].record(stream)
+            ml2.ml2_score_perf(p, X, pipe.valid, pipe.score, stream)
         if e is not None:
             e[2].record(stream)
         ml2.ml2_filter_topk(pipe.valid, pipe.score, w.k, pipe.idx, pipe.top, pipe.num, pipe.ws,
@@ -508,7 +547,8 @@ def main() -> int:
     num = int(pipe.num.item())
     _log(f"step {ms_per_step:.3f} ms (median of {args.steps}; mean {np.mean(steps_ms):.3f}, "
          f"wall {1000.0 * wall / args.steps:.3f}{' with MALL flushes' if flush is not None else ''}):"
-         f" validity {t_val:.3f} ms, perf {t_perf:.3f} ms, top-k {t_topk:.3f} ms"
+         + (f" validity + perf in one pass {t_val:.3f} ms" if fused else
+            f" validity {t_val:.3f} ms, perf {t_perf:.3f} ms") + f", top-k {t_topk:.3f} ms"
          + (f", re-rank {t_rerank:.3f} ms (kept {int(a_num.item())})" if second else "")
          + f"; valid {n_valid}/{w.n}, selected {num}")
     del flush
@@ -527,17 +567,21 @@ def main() -> int:
         _log(f"ragged P: {per_row / w.p_trees:.2f} splits per tree on average "
              f"(depth <= {w.p_depth})")
     sha = _kernel_sha()
+    if fused:  # one kernel walks V and P on every row
+        visits_p = w.n * (w.v_trees * w.v_depth + w.p_trees * w.p_depth)
+        t_perf = t_val
     perf_visits_per_s = visits_p / (t_perf / 1000.0)
     traffic = _traffic(sha) if w.name == "roofline" else None
     if w.name == "hbm":
         return _print(out_hbm(w, args, value, ms_per_step, t_val, t_perf, t_topk, n_valid,
-                              alg_bytes))
+                              alg_bytes, fused))
     shape = PERF_WALK_SHAPE.get(w.name)
     loop = walk_loop_ceiling(shape) * 1e12 if shape else None
     roofline = {
         "bound": "alu",
         "limiter": "lds",
-        "kernel": "perf_kernel (model P walk over accepted candidates)",
+        "kernel": ("fused_kernel (V then P on every row, one pass over the pool)" if fused
+                   else "perf_kernel (model P walk over accepted candidates)"),
         "peak_derivation": "node visits on chip (LDS + VALU, no HBM or MFMA term): LDS 256 "
                            "B/clk/CU x 256 CU x 2.4 GHz / 12 B per visit = "
                            f"{VISIT_PEAK_LDS / 1e12:.1f} T/s; VALU 128 lanes/clk/CU x 256 CU x "
@@ -549,8 +593,10 @@ def main() -> int:
         "frac": perf_visits_per_s / VISIT_PEAK_PER_S,
         "traffic": traffic,
         "traffic_unit": "bytes per launch (HBM read + write, copy-calibrated rocprofv3 counters)",
-        "work_per_launch": f"{visits_p} node visits ({n_valid} accepted x {w.p_trees} trees "
-                           + (f"x measured mean path)" if w.ragged else f"x depth {w.p_depth})"),
+        "work_per_launch": (f"{visits_p} node visits ({w.n} rows x ({w.v_trees} + {w.p_trees}) "
+                            f"trees x depth {w.p_depth})") if fused else
+                           (f"{visits_p} node visits ({n_valid} accepted x {w.p_trees} trees "
+                            + (f"x measured mean path)" if w.ragged else f"x depth {w.p_depth})")),
         "launch_ms": t_perf,
         "measured_ceiling": ({"achieved": loop / 1e12,
                               "frac": perf_visits_per_s / loop,
@@ -559,8 +605,9 @@ def main() -> int:
                                       f"lanes per candidate, {shape[3]} waves, {shape[4]} "
                                       "features; ml2_probe_visit, timed live)"}
                              if loop else None),
-        "validity_kernel": {"achieved": visits_v / (t_val / 1000.0) / 1e12, "launch_ms": t_val,
-                            "frac": visits_v / (t_val / 1000.0) / VISIT_PEAK_PER_S},
+        "validity_kernel": (None if fused else
+                            {"achieved": visits_v / (t_val / 1000.0) / 1e12, "launch_ms": t_val,
+                             "frac": visits_v / (t_val / 1000.0) / VISIT_PEAK_PER_S}),
         "hbm": {"algorithmic_bytes_per_step": alg_bytes,
                 "achieved_gbs": alg_bytes / (ms_per_step / 1000.0) / 1e9,
                 "peak_gbs": HBM_PEAK_GBS,
@@ -584,7 +631,8 @@ def main() -> int:
                              "validity_perf_features": f_vp}} if second else {}),
         "roofline": roofline,
         "hbm_frac": roofline["hbm"]["frac"],
-        "kernel_ms": {"validity": t_val, "perf": t_perf, "topk": t_topk,
+        "kernel_ms": {**({"validity_perf_one_pass": t_val} if fused else
+                         {"validity": t_val, "perf": t_perf}), "topk": t_topk,
                       **({"rerank": t_rerank} if second else {})},
     }
     del X

@@ -148,6 +148,25 @@ ml2_status ml2_score_validity(const ml2_ensemble *v, const float *X, int64_t n, 
 ml2_status ml2_score_perf(const ml2_ensemble *p, const float *X, int64_t n, int64_t ld,
                           const uint8_t *valid, float *score_out, void *stream);
 
+/*
+ * Validity and performance prediction in one call (models V and P of
+ * Section 2, "ML Model V" / "ML Model P"): the same outputs, bit for bit, as
+ * ml2_score_validity(v, X, n, ld, valid_out, margin_out) followed by
+ * ml2_score_perf(p, X, n, ld, valid_out, score_out).  Where both ensembles
+ * are perfect trees of one depth (at most 8) and fit one workgroup's LDS
+ * together, and the rows are 16-byte aligned with a multiple of 4 and at most
+ * 128 features, one kernel reads every row once and walks V and then P on
+ * it (P on every row, which costs nothing in HBM traffic; rejected rows
+ * still get -infinity); otherwise the two walks run one after the other.
+ * ml2_score_single_pass says which (1: one pass).  Arguments and errors as
+ * the two calls; X must hold the features of both ensembles.
+ */
+ml2_status ml2_score(const ml2_ensemble *v, const ml2_ensemble *p, const float *X, int64_t n,
+                     int64_t ld, uint8_t *valid_out, float *margin_out, float *score_out,
+                     void *stream);
+int32_t ml2_score_single_pass(const ml2_ensemble *v, const ml2_ensemble *p, const float *X,
+                              int64_t n, int64_t ld);
+
 /* Device workspace bytes ml2_filter_topk needs for (n, k).  Errors:
  * INVALID_ARG (NULL bytes, n < 0, k < 0), UNSUPPORTED (k > ML2_MAX_TOPK). */
 ml2_status ml2_topk_workspace_bytes(int64_t n, int32_t k, size_t *bytes);

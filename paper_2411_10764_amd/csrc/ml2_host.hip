@@ -548,6 +548,57 @@ ml2_status ml2_score_perf(const ml2_ensemble *p_ens, const float *X, int64_t n, 
   return ML2_OK;
 }
 
+namespace {
+
+ml2_status check_score_args(const ml2_ensemble *v, const ml2_ensemble *p, const float *X,
+                            int64_t n, int64_t ld, const void *valid_out, const void *score_out,
+                            const char *what, int *dev) {
+  ml2_status st = check_stream_args(v, X, n, ld, valid_out, what, dev);
+  if (st != ML2_OK) return st;
+  st = check_stream_args(p, X, n, ld, score_out, what, dev);
+  if (st != ML2_OK) return st;
+  return ML2_OK;
+}
+
+}  // namespace
+
+ml2_status ml2_score(const ml2_ensemble *v, const ml2_ensemble *p, const float *X, int64_t n,
+                     int64_t ld, uint8_t *valid_out, float *margin_out, float *score_out,
+                     void *stream) {
+  int dev = 0;
+  ml2_status st = check_score_args(v, p, X, n, ld, valid_out, score_out, "ml2_score", &dev);
+  if (st != ML2_OK) return st;
+  if (n == 0) return ML2_OK;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  ml2::WalkPlan pl;
+  int nv = 0, np = 0;
+  if (ml2::plan_fused(v->f, p->f, n, ld, X, cu_count(dev), &pl, &nv, &np)) {
+    hipError_t e = ml2::launch_fused(v->f, p->f, pl, nv, np, X, n, ld, valid_out, margin_out,
+                                     score_out, s);
+    if (e != hipSuccess) return hip_fail(e, "ml2_score: launch");
+    return ML2_OK;
+  }
+  ml2::WalkPlan pv, pp;
+  const char *why = nullptr;
+  if (!ml2::plan_walk(v->f, n, cu_count(dev), &pv, &why) ||
+      !ml2::plan_walk(p->f, n, cu_count(dev), &pp, &why))
+    return fail(ML2_ERR_UNSUPPORTED, "ml2_score: %s", why);
+  hipError_t e = ml2::launch_validity(v->f, pv, X, n, ld, valid_out, margin_out, s);
+  if (e == hipSuccess) e = ml2::launch_perf(p->f, pp, X, n, ld, valid_out, score_out, s);
+  if (e != hipSuccess) return hip_fail(e, "ml2_score: launch");
+  return ML2_OK;
+}
+
+int32_t ml2_score_single_pass(const ml2_ensemble *v, const ml2_ensemble *p, const float *X,
+                              int64_t n, int64_t ld) {
+  if (!v || !p || n < 1 || ld < v->f.num_features || ld < p->f.num_features) return 0;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  ml2::WalkPlan pl;
+  int nv = 0, np = 0;
+  return ml2::plan_fused(v->f, p->f, n, ld, X, cu_count(dev), &pl, &nv, &np) ? 1 : 0;
+}
+
 ml2_status ml2_topk_workspace_bytes(int64_t n, int32_t k, size_t *bytes) {
   if (!bytes) return fail(ML2_ERR_INVALID_ARG, "ml2_topk_workspace_bytes: bytes is NULL");
   if (n < 0 || n > (int64_t)INT32_MAX)

@@ -88,6 +88,16 @@ struct WalkPlan {
 // Returns false (and sets *why) if no plan fits the LDS of one workgroup.
 bool plan_walk(const Forest &f, int64_t n_work, int cu_count, WalkPlan *plan, const char **why);
 
+// Validity and performance in one pass over the pool (fused_kernel): false
+// where the two ensembles or the pool do not allow it.  nv, np: records of V
+// and P walked.
+constexpr int kMaxFusedDepth = 8;
+bool plan_fused(const Forest &v, const Forest &p, int64_t n, int64_t ld, const float *X,
+                int cu_count, WalkPlan *plan, int *nv, int *np);
+hipError_t launch_fused(const Forest &v, const Forest &p, const WalkPlan &pl, int nv, int np,
+                        const float *X, int64_t n, int64_t ld, uint8_t *valid_out,
+                        float *margin_out, float *score_out, hipStream_t s);
+
 // Tuning overrides (ml2_tune_walk_plan / ml2_tune_layout): process-wide,
 // zero = the planner's or loader's choice.
 enum TuneField { kTuneSplit, kTuneGroup, kTuneWaves, kTuneNbuf, kTuneChunk, kTuneLayout,

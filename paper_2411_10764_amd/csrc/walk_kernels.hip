@@ -89,6 +89,9 @@ struct WalkArgs {
   const int32_t *rows_in;   // row list: entry i is pool row rows_in[i]
   float *leaves_out;        // leaf walk of a row list: [fold_trees][n]
   int32_t fold_trees;       // trees (with padding trees) the fold adds up
+  const char *trees2;       // one pass over the pool: model P's records
+  int32_t ntrees2;          // its trees (V's are the first fold_trees of the list)
+  float base2;              // its margin bias
 };
 
 // Row `row` of X into the tile of its candidate (dst = tile + 4*candidate),
@@ -1195,6 +1198,118 @@ perf_kernel(WalkArgs a) {
   dispatch_rounds<S, RES>(a, rounds);
 }
 
+// Validity and performance in one pass over the pool (both ensembles
+// resident in LDS, perfect trees of one depth): each round loads the rows of
+// its tiles once and walks model V's trees followed by model P's on them as
+// one list of trees, in groups of G*S; each leaf is added to V's margin or
+// P's by its place in the list (V's trees first, in order, then P's), so
+// both folds keep tree order.  It writes the mask, the margin and the score
+// (-inf where V rejects; P is walked on every row, as the rows are on chip).
+// Rows are prefetched a round ahead as in the resident walks (the next
+// round's first batch before the walk, the second after the first group).
+// LDS: W tiles, then V's nv records, P's first trees, and -0.0 trees up to a
+// whole number of groups (ntrees records in all).
+template <int D, int G, int S, typename After>
+__device__ __forceinline__ float2 walk_split(const char *cb, int ntr, int nv,
+                                             const char *tile_lane, int h, float mv, float mp,
+                                             After after) {
+  constexpr uint32_t RB = record_bytes(D);
+  constexpr int GS = G * S;
+  constexpr int H = G == 1 ? 1 : G / 2;
+  auto add = [&](int t, float leaf) {
+    const bool to_v = t < nv;
+    mv = to_v ? mv + leaf : mv;
+    mp = to_v ? mp : mp + leaf;
+  };
+  for (int t0 = 0; t0 < ntr; t0 += GS) {
+    walk_group<D, G, S>(cb + (uint32_t)(t0 + h * G) * RB, tile_lane,
+                        [&](const auto &A, const auto &B) {
+      // this half's G trees t0 + h*G ..; the lower half adds its own, then
+      // the upper half's (they cross over by one lane swap per tree)
+      if constexpr (G == 1) {
+        add(t0, A.leaf[0]);
+        if constexpr (S == 2) add(t0 + 1, from_upper_half(A.leaf[0]));
+      } else {
+#pragma unroll
+        for (int g = 0; g < H; ++g) add(t0 + g, A.leaf[g]);
+#pragma unroll
+        for (int g = 0; g < H; ++g) add(t0 + H + g, B.leaf[g]);
+        if constexpr (S == 2) {
+#pragma unroll
+          for (int g = 0; g < H; ++g) add(t0 + G + g, from_upper_half(A.leaf[g]));
+#pragma unroll
+          for (int g = 0; g < H; ++g) add(t0 + G + H + g, from_upper_half(B.leaf[g]));
+        }
+      }
+    });
+    after(t0 / GS);
+  }
+  return make_float2(mv, mp);
+}
+
+template <int D, int G, int S>
+__global__ void __launch_bounds__(kLanes *kMaxWaves) __attribute__((amdgpu_waves_per_eu(S, S)))
+fused_kernel(WalkArgs a) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  constexpr uint32_t RB = record_bytes(D);
+  constexpr uint32_t L = 1u << D;
+  constexpr int CPW = Geo<S>::kCand;
+  const int lane = threadIdx.x & (kLanes - 1);
+  const int wave = threadIdx.x / kLanes;
+  const int h = lane / CPW;
+  const int cl = lane % CPW;
+  const int W = a.nthreads / kLanes;
+  const size_t tile_bytes = (size_t)a.F * Geo<S>::kRowBytes;
+  char *trees = smem + W * tile_bytes;
+  char *tile_lane = smem + wave * tile_bytes + 4 * cl;
+  {
+    // V's nv records, P's np records after them, then records of -0.0
+    // leaves (x + (-0.0) == x) up to ntrees
+    const int nv = a.fold_trees, np = a.ntrees2;
+    const uint32_t wv = (uint32_t)nv * (RB / 16u), wp = (uint32_t)np * (RB / 16u);
+    const uint32_t wall = (uint32_t)a.ntrees * (RB / 16u);
+    const u32x4 *sv = reinterpret_cast<const u32x4 *>(a.trees);
+    const u32x4 *sp = reinterpret_cast<const u32x4 *>(a.trees2);
+    u32x4 *d = reinterpret_cast<u32x4 *>(trees);
+    for (uint32_t i = threadIdx.x; i < wall; i += a.nthreads) {
+      u32x4 v;
+      if (i < wv) {
+        v = sv[i];
+      } else if (i < wv + wp) {
+        v = sp[i - wv];
+      } else {  // leaf j (L <= j < 2L) at byte 4L + 4j: bytes 8L .. 12L of the record
+        const uint32_t off = (i % (RB / 16u)) * 16u;
+        const uint32_t z = (off >= 8u * L && off < 12u * L) ? 0x80000000u : 0u;
+        v = u32x4{z, z, z, z};
+      }
+      d[i] = v;
+    }
+  }
+  constexpr int E = S == 2 ? 1 : 0;
+  RowPrefetch<S, E, S == 2, false> pf;
+  const int64_t ntiles = (a.n + CPW - 1) / CPW;
+  pf.load(a, ((int64_t)blockIdx.x * W + wave) * CPW + cl, h);
+  __syncthreads();
+  for (int64_t tg = blockIdx.x; tg * W < ntiles; tg += gridDim.x) {
+    const int64_t row = (tg * W + wave) * CPW + cl;
+    const bool active = row < a.n;
+    const int64_t rn = ((tg + gridDim.x) * W + wave) * CPW + cl;
+    pf.commit(a, row, h, tile_lane);
+    pf.template load_batch<0>(a, rn, h);
+    __syncthreads();
+    const float2 m = walk_split<D, G, S>(trees, a.ntrees, a.fold_trees, tile_lane, h, a.base,
+                                         a.base2,
+                                         [&](int g) { pf.load_after_group(a, rn, h, g); });
+    pf.load_rest(a, rn, h, (a.ntrees + G * S - 1) / (G * S));
+    if (active && h == 0) {
+      const bool ok = m.x > 0.0f;
+      __builtin_nontemporal_store((uint8_t)(ok ? 1 : 0), a.valid_out + row);
+      if (a.margin_out) __builtin_nontemporal_store(m.x, a.margin_out + row);
+      __builtin_nontemporal_store(ok ? m.y : -INFINITY, a.score_out + row);
+    }
+  }
+}
+
 // Tree-parallel walk of a short row list (the second level): workgroup
 // (c, r) stages tree chunk c once, loads list entries [r*64W, (r+1)*64W)
 // (lane = entry) and writes the leaf each of its trees gives each entry to
@@ -1519,7 +1634,125 @@ bool try_plan(const Forest &f, int64_t n_work, int cu_count, int S, int W, int m
   return true;
 }
 
+// One pass over the pool: depths 1..8, (G, S) with G*S dividing the tree
+// padding.
+template <int D, int G, int S>
+hipError_t launch_fused_dgs(const WalkPlan &p, const WalkArgs &a, hipStream_t s) {
+  static_assert(kTreePad % (G * S) == 0, "a walk group must divide the tree padding");
+  const void *fn = reinterpret_cast<const void *>(&fused_kernel<D, G, S>);
+  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     (int)p.lds_bytes);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((fused_kernel<D, G, S>), dim3(p.grid), dim3(p.waves * kLanes), p.lds_bytes,
+                     s, a);
+  return hipGetLastError();
+}
+
+template <int D, int S>
+hipError_t launch_fused_ds(const WalkPlan &p, const WalkArgs &a, hipStream_t s) {
+  switch (p.group) {
+    case 1: if constexpr (group_allowed(D, 1, S)) return launch_fused_dgs<D, 1, S>(p, a, s); break;
+    case 2: if constexpr (group_allowed(D, 2, S)) return launch_fused_dgs<D, 2, S>(p, a, s); break;
+    case 4: if constexpr (group_allowed(D, 4, S)) return launch_fused_dgs<D, 4, S>(p, a, s); break;
+    case 8: if constexpr (group_allowed(D, 8, S) && 8 * S <= kTreePad) return launch_fused_dgs<D, 8, S>(p, a, s); break;
+    default: break;
+  }
+  return hipErrorInvalidValue;
+}
+
+template <int D>
+hipError_t launch_fused_d(const WalkPlan &p, const WalkArgs &a, hipStream_t s) {
+  return p.split == 2 ? launch_fused_ds<D, 2>(p, a, s) : launch_fused_ds<D, 1>(p, a, s);
+}
+
 }  // namespace
+
+// One pass over the pool for V and P: both perfect, of one depth (at most
+// kMaxFusedDepth), rows prefetchable (16-byte aligned, F a multiple of 4,
+// at most 128 features), and the W candidate tiles plus both ensembles'
+// trees (their sum rounded up to a whole number of groups) within one
+// workgroup's LDS.  Shapes tried: eight waves with one lane per candidate,
+// eight with two, then four of each; larger groups first.  *nv: V's trees,
+// *np: P's trees staged (all of them).
+bool plan_fused(const Forest &v, const Forest &p, int64_t n, int64_t ld, const float *X,
+                int cu_count, WalkPlan *plan, int *nv, int *np) {
+  if (v.ragged || p.ragged || v.depth != p.depth || v.depth > kMaxFusedDepth) return false;
+  const int F = v.num_features > p.num_features ? v.num_features : p.num_features;
+  const bool vec4 = (reinterpret_cast<uintptr_t>(X) & 15u) == 0 && (ld & 3) == 0;
+  if (!vec4 || F % 4 != 0 || F > 4 * kRowVecs) return false;
+  const int D = v.depth;
+  const size_t rb = v.rec_bytes;
+  struct Shape { int s, w; };
+  const Shape shapes[] = {{1, 8}, {2, 8}, {1, 4}, {2, 4}};
+  for (const Shape &sh : shapes) {
+    for (int G : {8, 4, 2, 1}) {
+      const int gs = G * sh.s;
+      if (!group_allowed(D, G, sh.s) || kTreePad % gs != 0) continue;
+      const int all = (v.num_trees + p.num_trees + gs - 1) / gs * gs;
+      const size_t tile = (size_t)F * 4 * (kLanes / sh.s);
+      const size_t lds = (size_t)sh.w * tile + (size_t)all * rb;
+      if (lds > kLdsBudget) continue;
+      WalkPlan q{};
+      q.split = sh.s;
+      q.waves = sh.w;
+      q.group = G;
+      q.chunk_trees = all;
+      q.nbuf = 1;
+      q.lds_bytes = lds;
+      int per_cu = (int)(kLdsBudget / lds);
+      if (per_cu < 1) per_cu = 1;
+      if (per_cu > 8) per_cu = 8;
+      const int64_t tiles = (n + kLanes / sh.s - 1) / (kLanes / sh.s);
+      int64_t grid = (tiles + sh.w - 1) / sh.w;
+      if (grid > (int64_t)cu_count * per_cu) grid = (int64_t)cu_count * per_cu;
+      if (grid < 1) grid = 1;
+      q.grid = (int)grid;
+      *plan = q;
+      *nv = v.num_trees;
+      *np = p.num_trees;
+      return true;
+    }
+  }
+  return false;
+}
+
+hipError_t launch_fused(const Forest &v, const Forest &p, const WalkPlan &pl, int nv, int np,
+                        const float *X, int64_t n, int64_t ld, uint8_t *valid_out,
+                        float *margin_out, float *score_out, hipStream_t s) {
+  WalkArgs a{};
+  a.X = X;
+  a.n = n;
+  a.n_pool = n;
+  a.ld = ld;
+  a.trees = static_cast<const char *>(v.d_trees);
+  a.fold_trees = nv;  // V's trees: the first nv of the list
+  a.trees2 = static_cast<const char *>(p.d_trees);
+  a.ntrees2 = np;
+  a.ntrees = pl.chunk_trees;  // the list, padded to whole groups
+  a.chunk_trees = pl.chunk_trees;
+  a.nchunks = 1;
+  a.F = v.num_features > p.num_features ? v.num_features : p.num_features;
+  a.vec4 = 1;
+  a.nbuf = 1;
+  a.rowpf = 1;
+  a.nthreads = pl.waves * kLanes;
+  a.base = v.base;
+  a.base2 = p.base;
+  a.valid_out = valid_out;
+  a.margin_out = margin_out;
+  a.score_out = score_out;
+  switch (v.depth) {
+    case 1: return launch_fused_d<1>(pl, a, s);
+    case 2: return launch_fused_d<2>(pl, a, s);
+    case 3: return launch_fused_d<3>(pl, a, s);
+    case 4: return launch_fused_d<4>(pl, a, s);
+    case 5: return launch_fused_d<5>(pl, a, s);
+    case 6: return launch_fused_d<6>(pl, a, s);
+    case 7: return launch_fused_d<7>(pl, a, s);
+    case 8: return launch_fused_d<8>(pl, a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
 
 void set_tune(int field, int value) { g_tune[field].store(value, std::memory_order_relaxed); }
 int get_tune(int field) { return g_tune[field].load(std::memory_order_relaxed); }

@@ -30,7 +30,7 @@ ML2_MAX_STREAM_K = 4096
 EXPORTED = (
     "ml2_load_ensemble", "ml2_free_ensemble", "ml2_ensemble_num_features",
     "ml2_ensemble_num_trees", "ml2_ensemble_depth", "ml2_score_validity",
-    "ml2_score_perf", "ml2_topk_workspace_bytes", "ml2_filter_topk", "ml2_filter_topk_noalloc",
+    "ml2_score_perf", "ml2_score", "ml2_score_single_pass", "ml2_topk_workspace_bytes", "ml2_filter_topk", "ml2_filter_topk_noalloc",
     "ml2_rerank",
     "ml2_rerank_workspace_bytes",
     "ml2_explorer_create", "ml2_explorer_free", "ml2_explorer_reset", "ml2_explorer_rounds",
@@ -87,6 +87,10 @@ def lib():
         L.ml2_score_validity.argtypes = [P, P, I64, I64, P, P, P]
         L.ml2_score_perf.restype = I32
         L.ml2_score_perf.argtypes = [P, P, I64, I64, P, P, P]
+        L.ml2_score.restype = I32
+        L.ml2_score.argtypes = [P, P, P, I64, I64, P, P, P, P]
+        L.ml2_score_single_pass.restype = I32
+        L.ml2_score_single_pass.argtypes = [P, P, P, I64, I64]
         L.ml2_topk_workspace_bytes.restype = I32
         L.ml2_topk_workspace_bytes.argtypes = [I64, I32, ctypes.POINTER(SZ)]
         L.ml2_filter_topk.restype = I32
@@ -246,6 +250,20 @@ def ml2_score_perf(p: Ensemble, X, valid, score_out, stream=None) -> None:
     xp, n, ld = _rows(X)
     _check(lib().ml2_score_perf(p.handle, xp, n, ld, _ptr(valid), _ptr(score_out),
                                 _stream(stream)))
+
+
+def ml2_score(v: Ensemble, p: Ensemble, X, valid_out, margin_out, score_out,
+              stream=None) -> None:
+    """Validity and performance in one call (one pass over the pool where
+    the ensembles allow it)."""
+    xp, n, ld = _rows(X)
+    _check(lib().ml2_score(v.handle, p.handle, xp, n, ld, _ptr(valid_out), _ptr(margin_out),
+                           _ptr(score_out), _stream(stream)))
+
+
+def ml2_score_single_pass(v: Ensemble, p: Ensemble, X) -> bool:
+    xp, n, ld = _rows(X)
+    return bool(lib().ml2_score_single_pass(v.handle, p.handle, xp, n, ld))
 
 
 def ml2_topk_workspace_bytes(n: int, k: int) -> int:

@@ -202,6 +202,13 @@ def test_load_null_arguments():
     assert L.ml2_load_ensemble(ctypes.byref(d2), ctypes.byref(h)) == ml2.ML2_ERR_INVALID_ARG
 
 
+def test_score_one_call_rejects_null_ensembles():
+    L = ml2.lib()
+    P = 1 << 20  # never dereferenced
+    assert L.ml2_score(None, None, P, 10, 8, P, None, P, None) == ml2.ML2_ERR_INVALID_ARG
+    assert L.ml2_score_single_pass(None, None, P, 10, 8) == 0
+
+
 def test_score_calls_reject_null_ensemble():
     L = ml2.lib()
     assert L.ml2_score_validity(None, 4096, 10, 4, 8192, None, None) == ml2.ML2_ERR_INVALID_ARG
