@@ -13,7 +13,7 @@ with achieved node visits/s measured with HIP events on the launch stream.
 The `cpu_baseline` object times the CPU oracle (all host cores) on a
 bounded sample of the same pool.
 
-    python bench.py [--steps K] [--warmup W] [--workload NAME]
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--two-pass]
     python bench.py --copy-probe      # plain 1 GiB device copies (counter scale)
     python bench.py --probe           # LDS, VALU and walk-loop microbenchmarks
 """
@@ -59,7 +59,7 @@ MALL_BYTES = 256 << 20  # MI355X Infinity Cache: pools below it are flushed betw
 # per candidate, waves, features): the shape of the walk-loop probe.
 PERF_WALK_SHAPE = {"roofline": (8, 4, 2, 8, 128)}
 METRIC = "candidate configs scored+filtered/sec (validity+perf+top-k); % of HBM peak"
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "perf_walk_roofline_traffic.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "walk_traffic_16m.json")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2411_10764_amd", "csrc", "walk_kernels.hip")
 
 
@@ -72,9 +72,11 @@ def _kernel_sha() -> str:
         return hashlib.sha256(fh.read()).hexdigest()
 
 
-def _traffic(kernel_sha: str):
-    """HBM bytes per launch of the perf walk from committed rocprofv3 counter
-    runs, or None when absent or taken on a different kernel source."""
+def _traffic(kernel_sha: str, workload: str):
+    """HBM bytes per launch of the workload's dominant walk (the perf walk of
+    the 16M pool, the one-pass walk of the HBM diagnostic) from committed
+    rocprofv3 counter runs, or None when absent or taken on a different
+    kernel source."""
     try:
         with open(TRAFFIC_FILE) as fh:
             t = json.load(fh)
@@ -82,7 +84,7 @@ def _traffic(kernel_sha: str):
         return None
     if t.get("kernel_source_sha256") != kernel_sha:
         return None
-    return t.get("bytes_per_launch")
+    return t.get("launches", {}).get(workload, {}).get("bytes_per_launch")
 
 
 def copy_probe() -> None:
@@ -117,12 +119,16 @@ def probes() -> None:
     valu = ops / (ms * 1e-3)
     visit = {}
     # (depth, trees per lane, lanes per candidate, waves, features): the 16M
-    # pool's validity and perf walks first, then other shapes of depth 8
+    # pool's validity and perf walks first, then other shapes of depth 8,
+    # then the Skewed pool's perf walk (depth 10, 64 features) and shapes
+    # whose tiles and chunk also fit the LDS there
     shapes = [(6, 8, 2, 8, 128), (8, 4, 2, 8, 128), (8, 2, 2, 8, 128), (8, 4, 2, 4, 128),
-              (8, 8, 2, 4, 128), (8, 4, 2, 8, 64), (8, 8, 2, 8, 64), (8, 4, 1, 8, 64),
-              (8, 8, 1, 8, 64)]
+              (8, 8, 2, 4, 128), (8, 4, 2, 6, 128), (8, 8, 2, 6, 128), (8, 4, 2, 8, 64),
+              (8, 8, 2, 8, 64), (8, 4, 1, 8, 64), (8, 8, 1, 8, 64),
+              (10, 2, 1, 8, 64), (10, 1, 1, 8, 64), (10, 4, 1, 6, 64), (10, 4, 1, 4, 64),
+              (10, 1, 2, 8, 64), (10, 2, 2, 8, 64), (10, 4, 2, 6, 64), (10, 4, 2, 4, 64)]
     for d, g, s_, w, f in shapes:
-        ms, visits = ml2.ml2_probe_visit(d, g, s_, w, f, 512 if d == 8 else 1024, 4 * cus)
+        ms, visits = ml2.ml2_probe_visit(d, g, s_, w, f, {6: 1024, 8: 512, 10: 256}[d], 4 * cus)
         visit[f"D{d}_G{g}_S{s_}_W{w}_F{f}"] = round(visits / (ms * 1e-3) / 1e12, 3)
     print(json.dumps({
         "probe": "ml2_probe_*", "cus": cus, "clock_ghz_assumed": clk / 1e9,
@@ -340,7 +346,8 @@ def _print(out) -> int:
     return 0
 
 
-def out_hbm(w, args, value, ms_per_step, t_val, t_perf, t_topk, n_valid, alg_bytes, fused):
+def out_hbm(w, args, value, ms_per_step, t_val, t_perf, t_topk, n_valid, alg_bytes, fused,
+            traffic):
     """The HBM-bound diagnostic: small ensembles, so reading the pool bounds
     the step.  The roofline object covers the launch that reads every row
     once (4F bytes): with one pass the fused walk, which also writes the mask
@@ -364,7 +371,9 @@ def out_hbm(w, args, value, ms_per_step, t_val, t_perf, t_topk, n_valid, alg_byt
             "roofline": {
                 "bound": "hbm", "kernel": "fused_kernel (V then P on every row, one pass)",
                 "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                "traffic_unit": "bytes per launch (HBM read + write, copy-calibrated rocprofv3 "
+                                "counters)",
                 "work_per_launch": f"{f_bytes:.4g} bytes ({w.n} rows x {4 * w.F} B + mask + "
                                    "score)",
                 "launch_ms": t_val,
@@ -427,6 +436,9 @@ def main() -> int:
                     help="time ROUNDS explorer rounds over the pool streamed in row chunks "
                          "(resident slices and pinned-host copies)")
     ap.add_argument("--chunk-rows", type=int, default=1 << 21)
+    ap.add_argument("--two-pass", action="store_true",
+                    help="score with the validity walk and then the perf walk even where "
+                         "one pass over the pool fits")
     ap.add_argument("--N", type=int, default=10)
     ap.add_argument("--alpha", type=float, default=1.0)
     args = ap.parse_args()
@@ -486,7 +498,7 @@ def main() -> int:
     stream = torch.cuda.current_stream()
     # where both ensembles fit on chip together, ml2_score reads every row
     # once and walks V and P on it (one kernel); otherwise two walks
-    fused = ml2.ml2_score_single_pass(v, p, X)
+    fused = ml2.ml2_score_single_pass(v, p, X) and not args.two_pass
 
     def step(e=None):
         if e is not None:
@@ -571,10 +583,10 @@ def main() -> int:
         visits_p = w.n * (w.v_trees * w.v_depth + w.p_trees * w.p_depth)
         t_perf = t_val
     perf_visits_per_s = visits_p / (t_perf / 1000.0)
-    traffic = _traffic(sha) if w.name == "roofline" else None
+    traffic = _traffic(sha, w.name)
     if w.name == "hbm":
         return _print(out_hbm(w, args, value, ms_per_step, t_val, t_perf, t_topk, n_valid,
-                              alg_bytes, fused))
+                              alg_bytes, fused, traffic if fused else None))
     shape = PERF_WALK_SHAPE.get(w.name)
     loop = walk_loop_ceiling(shape) * 1e12 if shape else None
     roofline = {

@@ -31,10 +31,10 @@ extern "C" {
  * features per candidate, and a chunk of random perfect trees of depth
  * `depth` with `trees_per_lane` trees per lane, walked iters times (the
  * scoring walk's code without row loads or restaging).  *visits: node
- * visits made (candidates x trees x depth).  Built shapes: depth 6 or 8;
- * (trees_per_lane, lanes_per_candidate) (2, 2), (4, 2), (8, 2), (4, 1) or
- * (8, 1); waves 4 or 8; features 64 or 128; the tiles and the chunk within
- * one workgroup's LDS.  1 <= iters <= 2^20; 1 <= blocks <= 65536.  The 16M
+ * visits made (candidates x trees x depth).  Built shapes: depth 6, 8 or
+ * 10; trees_per_lane 1, 2, 4 or 8; lanes_per_candidate 1 or 2; waves 1 to
+ * 8; features 64 or 128; the tiles and the chunk within one workgroup's
+ * LDS.  1 <= iters <= 2^20; 1 <= blocks <= 65536.  The 16M
  * pool's walks: (6, 8, 2, 8, 128) and (8, 4, 2, 8, 128). */
 ml2_status ml2_probe_visit(int32_t depth, int32_t trees_per_lane, int32_t lanes_per_candidate,
                            int32_t waves, int32_t features, int32_t iters, int32_t blocks,

@@ -1088,9 +1088,9 @@ ml2_status ml2_probe_visit(int32_t depth, int32_t trees_per_lane, int32_t lanes_
   ml2_status st = check_probe("ml2_probe_visit", iters, blocks, ms, visits);
   if (st != ML2_OK) return st;
   const int G = trees_per_lane, S = lanes_per_candidate;
-  const bool shape_ok = (depth == 6 || depth == 8) &&
-                        ((S == 2 && (G == 2 || G == 4 || G == 8)) || (S == 1 && (G == 4 || G == 8))) &&
-                        (waves == 4 || waves == 8) && (features == 64 || features == 128);
+  const bool shape_ok = (depth == 6 || depth == 8 || depth == 10) &&
+                        (G == 1 || G == 2 || G == 4 || G == 8) && (S == 1 || S == 2) &&
+                        waves >= 1 && waves <= 8 && (features == 64 || features == 128);
   if (!shape_ok)
     return fail(ML2_ERR_INVALID_ARG,
                 "ml2_probe_visit: shape depth %d, %d trees per lane, %d lanes per candidate, %d "

@@ -13,6 +13,8 @@ constexpr int kProbeThreads = 256;
 constexpr uint32_t kProbeLds = 65536;         // bytes of LDS each workgroup reads
 constexpr uint32_t kProbeMask = kProbeLds - 16u;  // keeps every 16-byte read inside
 
+// 32-bit integer hash: the xorshift-multiply "lowbias32" constants found by
+// C. Wellons' hash-prospector search (2018).
 __device__ __forceinline__ uint32_t mix(uint32_t x) {
   x ^= x >> 16;
   x *= 0x7feb352du;

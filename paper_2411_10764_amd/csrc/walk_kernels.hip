@@ -58,9 +58,14 @@ struct Geo {
   static constexpr int kCand = kLanes / S;            // candidates per wave
   static constexpr uint32_t kRowBytes = 4u * kCand;   // one feature of a tile
   static constexpr int kRowShift = S == 1 ? 8 : 7;    // log2(kRowBytes)
-  static constexpr int kStageRegs = 6 / S;            // 16-byte registers per
-                                                      // thread for one chunk
 };
+
+// 16-byte registers per thread that stage one chunk: 6 / S, and 8 with one
+// lane per candidate for trees of depth 10 or more (12 KiB records), so that
+// six waves stage a chunk of four of them; such kernels keep two chunks in
+// registers instead of three (the register file holds no more).
+constexpr int stage_regs(int D, int S) { return (S == 1 && D >= 10) ? 8 : 6 / S; }
+constexpr int stage_sets(int D, int S, int sets) { return (S == 1 && D >= 10) ? 2 : sets; }
 
 struct WalkArgs {
   const float *X;
@@ -1042,7 +1047,8 @@ validity_kernel(WalkArgs a) {
   const int W = a.nthreads / kLanes;
   const size_t tile_bytes = (size_t)a.F * Geo<S>::kRowBytes;
   const uint32_t chunk_bytes = (uint32_t)a.chunk_trees * RB;
-  Stage<kValiditySets, Geo<S>::kStageRegs> st;
+  constexpr int K = stage_sets(D, S, kValiditySets);
+  Stage<K, stage_regs(D, S)> st;
   st.cur = smem + W * tile_bytes;
   st.other = st.cur + (a.nbuf == 2 ? chunk_bytes : 0u);
   char *tile_lane = smem + wave * tile_bytes + 4 * cl;
@@ -1052,7 +1058,7 @@ validity_kernel(WalkArgs a) {
     constexpr int M = decltype(mode)::value;
     // streamed ensembles (register staging): a second batch, loaded after
     // the first chunk
-    constexpr int E = M >= kResident ? row_extra_batches<S, kValiditySets, Geo<S>::kStageRegs>()
+    constexpr int E = M >= kResident ? row_extra_batches<S, K, stage_regs(D, S)>()
                       : (M == kStreamed && S == 2) ? 1
                                                    : 0;
     // lines shared by four lanes in the streamed kernel only (validity
@@ -1116,7 +1122,8 @@ perf_kernel(WalkArgs a) {
   const int cand = wave * CPW + cl;
   const size_t tile_bytes = (size_t)a.F * Geo<S>::kRowBytes;
   const uint32_t chunk_bytes = (uint32_t)a.chunk_trees * RB;
-  Stage<kPerfSets, Geo<S>::kStageRegs> st;
+  constexpr int K = stage_sets(D, S, kPerfSets);
+  Stage<K, stage_regs(D, S)> st;
   st.cur = smem + W * tile_bytes;
   st.other = st.cur + (a.nbuf == 2 ? chunk_bytes : 0u);
   int32_t *queue = reinterpret_cast<int32_t *>(st.other + chunk_bytes);  // C + NT entries
@@ -1161,7 +1168,7 @@ perf_kernel(WalkArgs a) {
   };
   auto rounds = [&](auto mode) {  // see validity_kernel
     constexpr int M = decltype(mode)::value;
-    constexpr int E = M >= kResident ? row_extra_batches<S, kPerfSets, Geo<S>::kStageRegs>() : 0;
+    constexpr int E = M >= kResident ? row_extra_batches<S, K, stage_regs(D, S)>() : 0;
     // lines shared by the halves in the resident kernel only (10 % faster
     // there; the streamed walk ran 0.4 % slower with it)
     RowPrefetch<S, E, RES && S == 2> pf;
@@ -1399,6 +1406,8 @@ constexpr bool group_allowed(int d, int g, int s) {
 
 // ---- visit probe -----------------------------------------------------------
 
+// 32-bit integer hash: the xorshift-multiply "lowbias32" constants found by
+// C. Wellons' hash-prospector search (2018).
 __device__ __forceinline__ uint32_t probe_hash(uint32_t x) {
   x ^= x >> 16;
   x *= 0x7feb352du;
@@ -1564,8 +1573,8 @@ hipError_t launch_leaves(int depth, const WalkArgs &a, int G, int W, size_t lds,
 
 std::atomic<int> g_tune[kTuneFields];
 
-size_t stage_reg_bytes(const WalkPlan &p) {
-  return (size_t)(6 / p.split) * 16 * kLanes * p.waves;
+size_t stage_reg_bytes(const WalkPlan &p, int depth) {
+  return (size_t)stage_regs(depth, p.split) * 16 * kLanes * p.waves;
 }
 
 WalkArgs make_args(const Forest &f, const WalkPlan &p, const float *X, int64_t n, int64_t ld) {
@@ -1581,7 +1590,10 @@ WalkArgs make_args(const Forest &f, const WalkPlan &p, const float *X, int64_t n
   a.F = f.num_features;
   a.vec4 = ((reinterpret_cast<uintptr_t>(X) & 15u) == 0 && (ld & 3) == 0) ? 1 : 0;
   a.nbuf = p.nbuf;
-  a.regstage = (p.nbuf == 1 && (size_t)p.chunk_trees * f.rec_bytes <= stage_reg_bytes(p)) ? 1 : 0;
+  a.regstage = (p.nbuf == 1 &&
+                 (size_t)p.chunk_trees * f.rec_bytes <= stage_reg_bytes(p, f.ragged ? 0 : f.depth))
+                    ? 1
+                    : 0;
   a.rowpf = (a.vec4 && (f.num_features % 4) == 0 && f.num_features <= 4 * kRowVecs) ? 1 : 0;
   a.nthreads = p.waves * kLanes;
   a.base = f.base;
@@ -1611,7 +1623,7 @@ bool try_plan(const Forest &f, int64_t n_work, int cu_count, int S, int W, int m
   q.split = S;
   q.waves = W;
   if (mode == 0) {  // the chunk must fit the staging registers
-    const int reg_trees = (int)(stage_reg_bytes(q) / rb) / gs * gs;
+    const int reg_trees = (int)(stage_reg_bytes(q, D) / rb) / gs * gs;
     if (reg_trees < gs) return false;
     if (chunk_trees > reg_trees) chunk_trees = reg_trees;
   }
@@ -1764,7 +1776,9 @@ int get_tune(int field) { return g_tune[field].load(std::memory_order_relaxed); 
 // (twice the candidates per pass over the ensemble), else two; then one lane
 // per candidate with four waves in the order register staging, two buffers,
 // synchronous copy; then fewer waves.  Larger G first within each (ragged
-// trees with one lane per candidate: smaller G first).  The tuning overrides
+// trees with one lane per candidate: smaller G first).  Deep perfect trees
+// with one lane per candidate take six waves of four trees per lane over
+// eight waves of fewer.  The tuning overrides
 // (ml2_tune_walk_plan) replace the choice where they fit; overrides that do
 // not fit are ignored.
 bool plan_walk(const Forest &f, int64_t n_work, int cu_count, WalkPlan *p, const char **why) {
@@ -1780,6 +1794,7 @@ bool plan_walk(const Forest &f, int64_t n_work, int cu_count, WalkPlan *p, const
   const int ragged_groups[5] = {1, 2, 4, 0, 0};
   struct Shape { int s, w; };
   const Shape shapes[] = {{1, 8}, {2, 8}, {1, 4}, {2, 4}, {1, 2}, {1, 1}};
+  const bool forced = want_s || want_g || want_w || want_b || want_c;
   for (int pass = 0; pass < 2; ++pass) {  // pass 0 honours the overrides
     for (const Shape &sh : shapes) {
       int S = sh.s, W = sh.w;
@@ -1794,7 +1809,16 @@ bool plan_walk(const Forest &f, int64_t n_work, int cu_count, WalkPlan *p, const
           if (pass == 0 && want_g && group_allowed(f.ragged ? 0 : f.depth, want_g, S) &&
               G != want_g)
             continue;
-          if (try_plan(f, n_work, cu_count, S, W, mode, G, pass == 0 ? want_c : 0, p)) return true;
+          if (!try_plan(f, n_work, cu_count, S, W, mode, G, pass == 0 ? want_c : 0, p)) continue;
+          // Deep perfect trees (12 KiB and more) with one lane per candidate:
+          // where eight tiles leave room for fewer than four trees per lane,
+          // six waves with four (a chunk twice as long, half the restaging
+          // per visit) are faster.
+          WalkPlan q;
+          if (!forced && !f.ragged && S == 1 && W == 8 && mode == 0 && G < 4 &&
+              try_plan(f, n_work, cu_count, 1, 6, 0, 4, 0, &q))
+            *p = q;
+          return true;
         }
       }
     }
@@ -1898,30 +1922,39 @@ hipError_t launch_visit_probe_dgs(int waves, int features, int iters, int blocks
 template <int D>
 hipError_t launch_visit_probe_d(int G, int S, int waves, int features, int iters, int blocks,
                                 float *out, double *visits, hipStream_t s) {
-  if (S == 2 && G == 2)
-    return launch_visit_probe_dgs<D, 2, 2>(waves, features, iters, blocks, out, visits, s);
-  if (S == 2 && G == 4)
-    return launch_visit_probe_dgs<D, 4, 2>(waves, features, iters, blocks, out, visits, s);
-  if (S == 2 && G == 8)
-    return launch_visit_probe_dgs<D, 8, 2>(waves, features, iters, blocks, out, visits, s);
-  if (S == 1 && G == 4)
-    return launch_visit_probe_dgs<D, 4, 1>(waves, features, iters, blocks, out, visits, s);
-  if (S == 1 && G == 8)
-    return launch_visit_probe_dgs<D, 8, 1>(waves, features, iters, blocks, out, visits, s);
+  if (S == 1) {
+    switch (G) {
+      case 1: return launch_visit_probe_dgs<D, 1, 1>(waves, features, iters, blocks, out, visits, s);
+      case 2: return launch_visit_probe_dgs<D, 2, 1>(waves, features, iters, blocks, out, visits, s);
+      case 4: return launch_visit_probe_dgs<D, 4, 1>(waves, features, iters, blocks, out, visits, s);
+      case 8: return launch_visit_probe_dgs<D, 8, 1>(waves, features, iters, blocks, out, visits, s);
+      default: break;
+    }
+  } else if (S == 2) {
+    switch (G) {
+      case 1: return launch_visit_probe_dgs<D, 1, 2>(waves, features, iters, blocks, out, visits, s);
+      case 2: return launch_visit_probe_dgs<D, 2, 2>(waves, features, iters, blocks, out, visits, s);
+      case 4: return launch_visit_probe_dgs<D, 4, 2>(waves, features, iters, blocks, out, visits, s);
+      case 8: return launch_visit_probe_dgs<D, 8, 2>(waves, features, iters, blocks, out, visits, s);
+      default: break;
+    }
+  }
   return hipErrorInvalidValue;
 }
 
-// The visit probe: depth 6 or 8; (G, S) one of (2, 2), (4, 2), (8, 2),
-// (4, 1), (8, 1); 4 or 8 waves; 64 or 128 features; the tiles and the chunk
-// must fit the LDS of one workgroup.  out: blocks * 512 floats.
+// The visit probe: depth 6, 8 or 10; G in {1, 2, 4, 8}, S in {1, 2}; 1 to 8
+// waves; 64 or 128 features; the tiles and the chunk must fit the LDS of one
+// workgroup.  out: blocks * 512 floats.
 hipError_t launch_visit_probe(int depth, int G, int S, int waves, int features, int iters,
                               int blocks, float *out, double *visits, hipStream_t s) {
-  if ((waves != 4 && waves != 8) || (features != 64 && features != 128))
+  if (waves < 1 || waves > kMaxWaves || (features != 64 && features != 128))
     return hipErrorInvalidValue;
   if (depth == 6)
     return launch_visit_probe_d<6>(G, S, waves, features, iters, blocks, out, visits, s);
   if (depth == 8)
     return launch_visit_probe_d<8>(G, S, waves, features, iters, blocks, out, visits, s);
+  if (depth == 10)
+    return launch_visit_probe_d<10>(G, S, waves, features, iters, blocks, out, visits, s);
   return hipErrorInvalidValue;
 }
 

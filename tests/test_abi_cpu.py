@@ -40,10 +40,12 @@ def test_exports_every_probe_symbol():
 
 
 @pytest.mark.parametrize("call", [
-    lambda L, ms, w: L.ml2_probe_visit(7, 4, 2, 8, 128, 10, 4, ms, w),    # depth 6 or 8
-    lambda L, ms, w: L.ml2_probe_visit(8, 2, 1, 8, 64, 10, 4, ms, w),     # shape not built
+    lambda L, ms, w: L.ml2_probe_visit(7, 4, 2, 8, 128, 10, 4, ms, w),    # depth 6, 8 or 10
+    lambda L, ms, w: L.ml2_probe_visit(8, 3, 1, 8, 64, 10, 4, ms, w),     # shape not built
+    lambda L, ms, w: L.ml2_probe_visit(8, 4, 4, 8, 64, 10, 4, ms, w),     # shape not built
     lambda L, ms, w: L.ml2_probe_visit(8, 8, 2, 8, 128, 10, 4, ms, w),    # beyond the LDS
-    lambda L, ms, w: L.ml2_probe_visit(8, 4, 2, 6, 128, 10, 4, ms, w),    # 4 or 8 waves
+    lambda L, ms, w: L.ml2_probe_visit(8, 4, 2, 9, 128, 10, 4, ms, w),    # 1 to 8 waves
+    lambda L, ms, w: L.ml2_probe_visit(8, 4, 2, 0, 128, 10, 4, ms, w),    # 1 to 8 waves
     lambda L, ms, w: L.ml2_probe_visit(8, 4, 2, 8, 128, 0, 4, ms, w),     # iters >= 1
     lambda L, ms, w: L.ml2_probe_visit(8, 4, 2, 8, 128, 10, 0, ms, w),    # blocks >= 1
     lambda L, ms, w: L.ml2_probe_visit(8, 4, 2, 8, 128, 10, 4, None, w),  # NULL output

@@ -55,12 +55,14 @@ def test_mall_flush_applies_to_pools_below_the_cache():
 def test_traffic_only_for_the_profiled_source(tmp_path, monkeypatch):
     sha = bench._kernel_sha()
     f = tmp_path / "traffic.json"
-    f.write_text(json.dumps({"kernel_source_sha256": sha, "bytes_per_launch": 123.0}))
+    f.write_text(json.dumps({"kernel_source_sha256": sha,
+                             "launches": {"roofline": {"bytes_per_launch": 123.0}}}))
     monkeypatch.setattr(bench, "TRAFFIC_FILE", str(f))
-    assert bench._traffic(sha) == 123.0
-    assert bench._traffic("0" * 64) is None  # counters taken on other source
+    assert bench._traffic(sha, "roofline") == 123.0
+    assert bench._traffic(sha, "hbm") is None  # no counters for that workload
+    assert bench._traffic("0" * 64, "roofline") is None  # counters taken on other source
     monkeypatch.setattr(bench, "TRAFFIC_FILE", str(tmp_path / "missing.json"))
-    assert bench._traffic(sha) is None
+    assert bench._traffic(sha, "roofline") is None
 
 
 def test_committed_traffic_matches_current_source():
@@ -72,6 +74,8 @@ def test_committed_traffic_matches_current_source():
     if t["kernel_source_sha256"] != bench._kernel_sha():
         pytest.skip("walk kernels changed since the counters were taken (traffic reported null)")
     copy = t["copy_probe"]
-    want = (t["fetch_size_kib"] * 1024 / copy["fetch_factor"]
-            + t["write_size_kib"] * 1024 / copy["write_factor"])
-    assert t["bytes_per_launch"] == pytest.approx(want, rel=1e-9)
+    assert set(t["launches"]) == {"roofline", "hbm"}
+    for launch in t["launches"].values():
+        want = (launch["fetch_size_kib"] * 1024 / copy["fetch_factor"]
+                + launch["write_size_kib"] * 1024 / copy["write_factor"])
+        assert launch["bytes_per_launch"] == pytest.approx(want, rel=1e-9)

@@ -204,6 +204,7 @@ def test_depth_and_width_limits(depth, F, trees):
     (1, 4, 4, 1, 0, 7), (1, 8, 8, 1, 0, 7), (1, 8, 4, 2, 0, 7), (1, 8, 4, 1, 16, 7),
     (2, 8, 8, 1, 0, 7), (2, 4, 8, 1, 16, 7), (2, 4, 4, 1, 0, 7), (2, 8, 8, 1, 32, 7),
     (2, 4, 8, 1, 16, 6), (2, 2, 8, 1, 0, 8), (2, 1, 8, 1, 0, 9), (2, 1, 8, 1, 0, 10),
+    (1, 4, 6, 1, 0, 10), (1, 2, 8, 1, 0, 10), (1, 4, 8, 1, 0, 10), (1, 2, 6, 1, 0, 11),
 ])
 def test_walk_plans(tune, split, group, waves, nbuf, chunk, depth):
     """Every launch shape of the walks (lanes per candidate, trees per lane,

@@ -11,7 +11,8 @@ from paper_2411_10764_amd import ml2  # noqa: E402
 
 @pytest.mark.parametrize("depth,G,S,waves,F", [
     (6, 8, 2, 8, 128), (8, 4, 2, 8, 128), (8, 2, 2, 8, 128), (8, 8, 2, 8, 64), (8, 8, 2, 4, 128),
-    (8, 4, 1, 8, 64), (8, 8, 1, 8, 64), (6, 4, 2, 4, 64)])
+    (8, 4, 1, 8, 64), (8, 8, 1, 8, 64), (6, 4, 2, 4, 64), (10, 2, 1, 8, 64), (10, 4, 1, 6, 64),
+    (10, 1, 2, 8, 64), (10, 4, 2, 6, 64), (8, 8, 2, 6, 128)])
 def test_visit_probe(depth, G, S, waves, F):
     ms, visits = ml2.ml2_probe_visit(depth, G, S, waves, F, 4, 8)
     assert visits == 8 * waves * (64 // S) * 4 * (G * S) * depth
