@@ -14,7 +14,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libml2.so")
-SOURCES = ["ml2_host.hip", "walk_kernels.hip", "topk_kernels.hip", "probe_kernels.hip"]
+SOURCES = ["ml2_host.hip", "walk_kernels.hip", "topk_kernels.hip", "probe_kernels.hip", "pack.cpp"]
 ARCH = os.environ.get("ML2_OFFLOAD_ARCH", "gfx950")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

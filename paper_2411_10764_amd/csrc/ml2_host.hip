@@ -15,6 +15,13 @@
 #include <vector>
 
 #include "ml2_internal.h"
+#include "pack.h"
+
+using ml2::pack_ragged;
+using ml2::pad_identity_tree;
+using ml2::pad_tree;
+using ml2::RaggedPack;
+using ml2::TreeView;
 #include "ml2_probe.h"
 
 struct ml2_ensemble {
@@ -105,14 +112,7 @@ ml2_status current_device(int *dev) {
   return ML2_OK;
 }
 
-// ---- descriptor validation and padding ------------------------------------
-
-struct TreeView {
-  const int32_t *left, *right, *feat;
-  const float *thr, *val;
-  const uint8_t *dl;  // NULL: every missing value goes right
-  int64_t size;
-};
+// ---- descriptor validation ------------------------------------------------
 
 // Checks that tree t is a proper binary tree rooted at 0 and returns its depth.
 ml2_status check_tree(const ml2_ensemble_desc &d, int32_t t, const TreeView &tv, int *depth_out,
@@ -162,153 +162,6 @@ ml2_status check_tree(const ml2_ensemble_desc &d, int32_t t, const TreeView &tv,
   return ML2_OK;
 }
 
-// Fill the perfect-tree record of depth D from the general tree (replicating
-// leaves that sit above depth D into dummy subtrees).
-void pad_tree(const TreeView &tv, int D, char *rec) {
-  const uint32_t L = 1u << D;
-  uint2 *nodes = reinterpret_cast<uint2 *>(rec);              // nodes[j], 1 <= j < L
-  float *leaves = reinterpret_cast<float *>(rec + 4u * L);    // leaves[j], L <= j < 2L
-  struct Item {
-    int32_t node;
-    uint32_t pos;
-  };
-  std::vector<Item> stack;
-  stack.push_back({0, 1u});
-  while (!stack.empty()) {
-    const Item it = stack.back();
-    stack.pop_back();
-    const bool leaf = tv.left[it.node] == -1 && tv.right[it.node] == -1;
-    if (it.pos >= L) {  // only leaves reach depth D
-      leaves[it.pos] = tv.val[it.node];
-      continue;
-    }
-    if (leaf) {
-      nodes[it.pos] = make_uint2(0u, 0u);  // feature 0, threshold +0: both sides equal
-      stack.push_back({it.node, 2 * it.pos});
-      stack.push_back({it.node, 2 * it.pos + 1});
-    } else {
-      uint32_t tb;
-      memcpy(&tb, &tv.thr[it.node], 4);
-      nodes[it.pos] = make_uint2((uint32_t)tv.feat[it.node], tb);
-      stack.push_back({tv.left[it.node], 2 * it.pos + 1});
-      stack.push_back({tv.right[it.node], 2 * it.pos});
-    }
-  }
-}
-
-// ---- ragged layout ---------------------------------------------------------
-
-// Pack trees (breadth-first renumbered: siblings adjacent) into fixed chunk
-// slots (format in ml2_internal.h).  Returns the number of slots and the
-// total tree count with the padding trees.
-struct RaggedPack {
-  std::vector<char> bytes;
-  int32_t slots = 0;
-  int32_t trees = 0;
-  int32_t depth = 0;
-};
-
-void pack_ragged(const std::vector<TreeView> &views, const std::vector<int> &depths,
-                 RaggedPack *out) {
-  constexpr uint32_t CAP = ml2::kRaggedChunkBytes;
-  constexpr int GRP = ml2::kRaggedGroup;
-  // a leaf's first word: offset -1 (the node itself) and, in the low half,
-  // the byte offset in the slot of the next tree's root (the sentinel after
-  // the last tree)
-  auto leaf_word0 = [](uint32_t next_root) { return (0x7FFFu << 16) | (8u * next_root); };
-  auto bits = [](float v) {
-    uint32_t b;
-    memcpy(&b, &v, 4);
-    return b;
-  };
-  size_t t = 0;
-  int32_t tree_index = 0;
-  while (t < views.size()) {
-    // choose the trees of this slot: header + roots + 8 bytes per node,
-    // with room left for padding the tree count to a multiple of GRP
-    size_t first = t, nodes = 0;
-    // (two more root entries and one more node: the sentinel)
-    auto need = [&](size_t ntrees, size_t nnodes) {
-      const size_t ntr = (ntrees + GRP - 1) / GRP * GRP;
-      const size_t head = (16 + 4 * (ntr + 2) + 15) & ~(size_t)15;
-      return head + 8 * (nnodes + (ntr - ntrees) + 1);
-    };
-    while (t < views.size() && need(t + 1 - first, nodes + (size_t)views[t].size) <= CAP) {
-      nodes += (size_t)views[t].size;
-      ++t;
-    }
-    const size_t real = t - first;
-    const size_t ntr = (real + GRP - 1) / GRP * GRP;
-    const size_t all_nodes = nodes + (ntr - real);
-    const uint32_t head = (uint32_t)((16 + 4 * (ntr + 2) + 15) & ~(size_t)15);
-    const size_t slot0 = out->bytes.size();
-    out->bytes.resize(slot0 + CAP, 0);
-    char *slot = out->bytes.data() + slot0;
-    uint32_t *root = reinterpret_cast<uint32_t *>(slot + 16);
-    uint2 *node = reinterpret_cast<uint2 *>(slot + head);
-    int depth = 0;
-    uint32_t next = 0;  // next free node index in the slot
-    std::vector<int32_t> order;
-    for (size_t i = 0; i < ntr; ++i) {
-      root[i] = head / 8u + next;
-      if (i >= real) {  // padding: one leaf of value -0.0
-        node[next] = make_uint2(leaf_word0(head / 8u + next + 1), bits(-0.0f));
-        ++next;
-        continue;
-      }
-      const TreeView &tv = views[first + i];
-      if (depths[first + i] > depth) depth = depths[first + i];
-      // breadth-first ids: order[k] = original node of new id k
-      order.assign(1, 0);
-      std::vector<int32_t> newid((size_t)tv.size, -1);
-      newid[0] = 0;
-      for (size_t k = 0; k < order.size(); ++k) {
-        const int32_t o = order[k];
-        if (tv.left[o] == -1) continue;
-        newid[(size_t)tv.left[o]] = (int32_t)order.size();
-        order.push_back(tv.left[o]);
-        newid[(size_t)tv.right[o]] = (int32_t)order.size();
-        order.push_back(tv.right[o]);
-      }
-      for (size_t k = 0; k < order.size(); ++k) {
-        const int32_t o = order[k];
-        const uint32_t j = next + (uint32_t)k;
-        if (tv.left[o] == -1) {
-          node[j] = make_uint2(leaf_word0(head / 8u + next + (uint32_t)order.size()),
-                               bits(tv.val[o]));
-        } else {
-          const int32_t rel = newid[(size_t)tv.left[o]] - (int32_t)k;  // nodes, > 0
-          const uint32_t dl = (tv.dl && tv.dl[o]) ? 1u : 0u;
-          uint32_t tb;
-          memcpy(&tb, &tv.thr[o], 4);
-          node[j] = make_uint2((dl << 31) | (((uint32_t)rel & 0x7FFFu) << 16) |
-                                   ((uint32_t)tv.feat[o] << 8),
-                               tb);
-        }
-      }
-      next += (uint32_t)order.size();
-    }
-    // the sentinel: a leaf of value -0.0 that the two entries after the last
-    // root point to (a walk past its last tree moves onto it; adding -0.0
-    // changes no float)
-    const uint32_t sentinel = head / 8u + next;
-    node[next] = make_uint2(leaf_word0(sentinel), bits(-0.0f));
-    root[ntr] = root[ntr + 1] = sentinel;
-    ++next;
-    const uint32_t hdr[4] = {(uint32_t)ntr, (uint32_t)depth, sentinel, (uint32_t)tree_index};
-    memcpy(slot, hdr, sizeof hdr);
-    tree_index += (int32_t)ntr;
-    if (depth > out->depth) out->depth = depth;
-    out->slots += 1;
-  }
-  out->trees = tree_index;
-}
-
-void pad_identity_tree(int D, char *rec) {  // every leaf -0.0
-  const uint32_t L = 1u << D;
-  float *leaves = reinterpret_cast<float *>(rec + 4u * L);
-  for (uint32_t j = L; j < 2 * L; ++j) leaves[j] = -0.0f;
-}
 
 ml2_status check_stream_args(const ml2_ensemble *e, const float *X, int64_t n, int64_t ld,
                              const void *out, const char *what, int *dev) {
