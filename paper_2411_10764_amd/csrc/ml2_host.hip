@@ -12,6 +12,7 @@
 #include <mutex>
 #include <new>
 #include <string>
+#include <unordered_map>
 #include <vector>
 
 #include "ml2_internal.h"
@@ -224,6 +225,27 @@ ml2_status check_probe(const char *what, int32_t iters, int32_t blocks, const do
 }
 
 }  // namespace
+
+namespace ml2 {
+
+hipError_t ensure_dynamic_lds(const void *fn, size_t bytes) {
+  static std::mutex mu;
+  static std::unordered_map<const void *, std::vector<size_t>> set;  // per kernel, per device
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lock(mu);
+  std::vector<size_t> &v = set[fn];
+  if ((int)v.size() <= dev) v.resize((size_t)dev + 1, 0);
+  if (bytes > v[(size_t)dev]) {
+    e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    if (e != hipSuccess) return e;
+    v[(size_t)dev] = bytes;
+  }
+  return hipSuccess;
+}
+
+}  // namespace ml2
 
 extern "C" {
 

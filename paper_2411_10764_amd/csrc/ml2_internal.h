@@ -13,6 +13,12 @@ namespace ml2 {
 constexpr size_t kLdsBudget = 160 * 1024 - 256;  // LDS of a walk workgroup (static LDS headroom)
 constexpr size_t kTreeSlack = 128 * 1024;  // readable zero bytes after the tree table
 
+// hipFuncSetAttribute(MaxDynamicSharedMemorySize) for kernel fn on the current
+// device, called only when `bytes` exceeds what was set there before (the
+// launchers call it before every launch; the attribute call itself then runs
+// once per kernel, device and size increase).
+hipError_t ensure_dynamic_lds(const void *fn, size_t bytes);
+
 struct Forest {
   int device;
   int32_t num_trees;        // trees in the descriptor

@@ -884,23 +884,6 @@ hipError_t barrier_ticks(long long *ticks) {
   return hipSuccess;
 }
 
-// hipFuncSetAttribute once per kernel, device and LDS size above the largest set so far.
-hipError_t ensure_lds(const void *fn, int slot, size_t bytes) {
-  static std::mutex mu;
-  static std::vector<size_t> set[4];
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return e;
-  std::lock_guard<std::mutex> lock(mu);
-  std::vector<size_t> &v = set[slot];
-  if ((int)v.size() <= dev) v.resize((size_t)dev + 1, 0);
-  if (bytes > v[(size_t)dev]) {
-    e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
-    if (e != hipSuccess) return e;
-    v[(size_t)dev] = bytes;
-  }
-  return hipSuccess;
-}
 
 }  // namespace
 
@@ -917,7 +900,7 @@ hipError_t launch_topk(const uint8_t *valid, const float *scores, int64_t n, int
     const size_t lds =
         ((size_t)sort_size(min((int64_t)k, n)) + (size_t)(n > 0 ? n : 1)) * sizeof(unsigned long long);
     const size_t most = ((size_t)sort_size(kSmallN) + kSmallN) * sizeof(unsigned long long);
-    hipError_t e = ensure_lds(reinterpret_cast<const void *>(&topk_small), 3, most);
+    hipError_t e = ensure_dynamic_lds(reinterpret_cast<const void *>(&topk_small), most);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(topk_small, dim3(1), dim3(kSortThreads), lds, s, valid, scores, n, k, idx,
                        score, num);
@@ -944,7 +927,7 @@ hipError_t launch_topk(const uint8_t *valid, const float *scores, int64_t n, int
     if (e != hipSuccess) return e;
   }
   const size_t lds = (size_t)sort_size(k) * sizeof(unsigned long long);
-  e = ensure_lds(reinterpret_cast<const void *>(&topk_finish), 0, lds);
+  e = ensure_dynamic_lds(reinterpret_cast<const void *>(&topk_finish), lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(topk_finish, dim3(1), dim3(kSortThreads), lds, s, scores, n, st, take,
                      inbin, idx, score, num);
@@ -955,7 +938,7 @@ hipError_t launch_rerank_select(const int32_t *rows, const float *scores, int32_
                                 int32_t keep, int32_t *idx, float *score, int32_t *num,
                                 hipStream_t s) {
   const size_t lds = (size_t)sort_size(m) * sizeof(unsigned long long);
-  hipError_t e = ensure_lds(reinterpret_cast<const void *>(&rerank_select), 1, lds);
+  hipError_t e = ensure_dynamic_lds(reinterpret_cast<const void *>(&rerank_select), lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(rerank_select, dim3(1), dim3(kSortThreads), lds, s, rows, scores, m, n, keep,
                      idx, score, num);
@@ -996,7 +979,7 @@ hipError_t launch_merge_held(const int32_t *h_id, const float *h_p, const float 
                              const float *c_a, const int32_t *c_n, int64_t row0, int32_t k,
                              int32_t *o_id, float *o_p, float *o_a, int32_t *o_n, hipStream_t s) {
   const size_t lds = merge_held_lds(k);
-  hipError_t e = ensure_lds(reinterpret_cast<const void *>(&merge_held), 2, lds);
+  hipError_t e = ensure_dynamic_lds(reinterpret_cast<const void *>(&merge_held), lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(merge_held, dim3(1), dim3(kSortThreads), lds, s, h_id, h_p, h_a, h_n, c_idx,
                      c_p, c_a, c_n, row0, k, o_id, o_p, o_a, o_n);

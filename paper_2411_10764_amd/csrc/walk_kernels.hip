@@ -377,7 +377,7 @@ struct RWalks {
   __device__ __forceinline__ static bool is_leaf(uint32_t w0) { return (w0 >> 16) == 0x7FFFu; }
 };
 
-// Ragged chunk slot header (see ml2_internal.h), read from LDS into scalars.
+// Ragged chunk slot header (layout.h), read from LDS into scalars.
 struct SlotHead {
   int ntrees;
   int depth;
@@ -1462,8 +1462,7 @@ template <int D, int G, int S, bool RES>
 hipError_t launch_kernel(bool perf, const WalkPlan &p, const WalkArgs &a, hipStream_t s) {
   const void *fn = perf ? reinterpret_cast<const void *>(&perf_kernel<D, G, S, RES>)
                         : reinterpret_cast<const void *>(&validity_kernel<D, G, S, RES>);
-  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                     (int)p.lds_bytes);
+  hipError_t e = ensure_dynamic_lds(fn, p.lds_bytes);
   if (e != hipSuccess) return e;
   dim3 grid(p.grid), block(p.waves * kLanes);
   if (perf)
@@ -1530,7 +1529,7 @@ hipError_t launch_walk(bool perf, const Forest &f, const WalkPlan &p, const Walk
 template <int D, int G>
 hipError_t launch_leaves_dg(const WalkArgs &a, int W, size_t lds, int row_tiles, hipStream_t s) {
   const void *fn = reinterpret_cast<const void *>(&leaves_kernel<D, G>);
-  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  hipError_t e = ensure_dynamic_lds(fn, lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((leaves_kernel<D, G>), dim3((unsigned)a.nchunks, (unsigned)row_tiles),
                      dim3(W * kLanes), lds, s, a);
@@ -1652,8 +1651,7 @@ template <int D, int G, int S>
 hipError_t launch_fused_dgs(const WalkPlan &p, const WalkArgs &a, hipStream_t s) {
   static_assert(kTreePad % (G * S) == 0, "a walk group must divide the tree padding");
   const void *fn = reinterpret_cast<const void *>(&fused_kernel<D, G, S>);
-  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                     (int)p.lds_bytes);
+  hipError_t e = ensure_dynamic_lds(fn, p.lds_bytes);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((fused_kernel<D, G, S>), dim3(p.grid), dim3(p.waves * kLanes), p.lds_bytes,
                      s, a);
@@ -1910,7 +1908,7 @@ hipError_t launch_visit_probe_dgs(int waves, int features, int iters, int blocks
   const size_t lds =
       (size_t)waves * features * Geo<S>::kRowBytes + (size_t)G * S * record_bytes(D);
   if (lds > kLdsBudget) return hipErrorInvalidValue;
-  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  hipError_t e = ensure_dynamic_lds(fn, lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((visit_probe_kernel<D, G, S>), dim3(blocks), dim3(waves * kLanes), lds, s,
                      out, iters, features, waves);
