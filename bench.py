@@ -13,7 +13,7 @@ with achieved node visits/s measured with HIP events on the launch stream.
 The `cpu_baseline` object times the CPU oracle (all host cores) on a
 bounded sample of the same pool.
 
-    python bench.py [--steps K] [--warmup W] [--workload NAME] [--two-pass]
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--two-pass] [--graph]
     python bench.py --copy-probe      # plain 1 GiB device copies (counter scale)
     python bench.py --probe           # LDS, VALU and walk-loop microbenchmarks
 """
@@ -436,6 +436,8 @@ def main() -> int:
                     help="time ROUNDS explorer rounds over the pool streamed in row chunks "
                          "(resident slices and pinned-host copies)")
     ap.add_argument("--chunk-rows", type=int, default=1 << 21)
+    ap.add_argument("--graph", action="store_true",
+                    help="time the step as a captured HIP graph, replayed once per step")
     ap.add_argument("--two-pass", action="store_true",
                     help="score with the validity walk and then the perf walk even where "
                          "one pass over the pool fits")
@@ -500,29 +502,29 @@ def main() -> int:
     # once and walks V and P on it (one kernel); otherwise two walks
     fused = ml2.ml2_score_single_pass(v, p, X) and not args.two_pass
 
-    def step(e=None):
+    def step(e=None, s=stream):  # s None: the current stream (a graph capture's)
         if e is not None:
-            e[0].record(stream)
+            e[0].record(s)
         if fused:
-            ml2.ml2_score(v, p, X, pipe.valid, None, pipe.score, stream)
+            ml2.ml2_score(v, p, X, pipe.valid, None, pipe.score, s)
             if e is not None:
-                e[1].record(stream)
+                e[1].record(s)
         else:
-            ml2.ml2_score_validity(v, X, pipe.valid, None, stream)
+            ml2.ml2_score_validity(v, X, pipe.valid, None, s)
             if e is not None:
-                e[1].record(stream)
-            ml2.ml2_score_perf(p, X, pipe.valid, pipe.score, stream)
+                e[1].record(s)
+            ml2.ml2_score_perf(p, X, pipe.valid, pipe.score, s)
         if e is not None:
-            e[2].record(stream)
+            e[2].record(s)
         ml2.ml2_filter_topk(pipe.valid, pipe.score, w.k, pipe.idx, pipe.top, pipe.num, pipe.ws,
-                            pipe.ws_bytes, w.n, stream)
+                            pipe.ws_bytes, w.n, s)
         if e is not None:
-            e[3].record(stream)
+            e[3].record(s)
         if second:
             ml2.ml2_rerank(a, X, pipe.idx, w.keep, a_scores, a_idx, a_top, a_num, a_ws, a_wsb,
-                           m=w.k, stream=stream)
+                           m=w.k, stream=s)
         if e is not None:
-            e[4].record(stream)
+            e[4].record(s)
 
     # Pools that fit the 256 MB MALL are flushed before every step (a 512 MB
     # read-modify-write on the same stream, outside the timed events), so
@@ -554,6 +556,27 @@ def main() -> int:
     t_rerank = float(np.median([e[3].elapsed_time(e[4]) for e in ev]))
     steps_ms = [e[0].elapsed_time(e[4]) for e in ev]
     ms_per_step = float(np.median(steps_ms))
+    eager_ms = ms_per_step
+    if args.graph:
+        # the step captured once as a HIP graph and replayed: the same
+        # launches, without the host's per-launch work between them; the
+        # kernel split above is that of the eager steps
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step(None, None)
+        torch.cuda.synchronize()
+        gev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+        for s in range(args.steps):
+            if flush is not None:
+                flush.add_(1.0)
+            gev[s][0].record(stream)
+            g.replay()
+            gev[s][1].record(stream)
+        torch.cuda.synchronize()
+        ms_per_step = float(np.median([e[0].elapsed_time(e[1]) for e in gev]))
+        _log(f"graph replays: {ms_per_step:.3f} ms per step (median of {args.steps}; eager "
+             f"{eager_ms:.3f} ms)")
+        del g
     valid = pipe.valid.cpu().numpy()
     n_valid = int(valid.sum())
     num = int(pipe.num.item())
@@ -566,6 +589,7 @@ def main() -> int:
     del flush
 
     value = w.n / (ms_per_step / 1000.0)
+    launch = ({"launch": "hip_graph", "eager_ms_per_step": eager_ms} if args.graph else {})
     f_vp = w.K if w.visible_only else w.F
     alg_bytes = 4.0 * f_vp * w.n + w.n + 8.0 * w.k
     if second:
@@ -585,8 +609,10 @@ def main() -> int:
     perf_visits_per_s = visits_p / (t_perf / 1000.0)
     traffic = _traffic(sha, w.name)
     if w.name == "hbm":
-        return _print(out_hbm(w, args, value, ms_per_step, t_val, t_perf, t_topk, n_valid,
-                              alg_bytes, fused, traffic if fused else None))
+        res = out_hbm(w, args, value, ms_per_step, t_val, t_perf, t_topk, n_valid, alg_bytes,
+                      fused, traffic if fused else None)
+        res["config"].update(launch)
+        return _print(res)
     shape = PERF_WALK_SHAPE.get(w.name)
     loop = walk_loop_ceiling(shape) * 1e12 if shape else None
     roofline = {
@@ -637,7 +663,7 @@ def main() -> int:
                    "perf": f"{w.p_trees} trees x depth {'<= ' if w.ragged else ''}{w.p_depth}"
                            + (" (ragged, default directions)" if w.ragged else ""),
                    "k": w.k, "missing_hidden_fraction": w.missing,
-                   "seed": w.seed, "invalid_fraction": 1 - n_valid / w.n},
+                   "seed": w.seed, "invalid_fraction": 1 - n_valid / w.n, **launch},
         **({"second_level": {"model_a": f"{w.a_trees} trees x depth {w.a_depth} over {w.F} "
                                         f"features", "keep": w.keep,
                              "validity_perf_features": f_vp}} if second else {}),
