@@ -1606,7 +1606,9 @@ bool try_plan(const Forest &f, int64_t n_work, int cu_count, int S, int W, int m
               int want_c, WalkPlan *p) {
   const int D = f.ragged ? 0 : f.depth;
   if (!group_allowed(D, G, S) || W < 1 || W > kMaxWaves) return false;
-  if (S == 2 && mode != 0) return false;  // groups are sized for register staging
+  // two lanes per candidate: register staging only (two buffers filled by
+  // direct global-to-LDS copies were 12 to 75 % slower where they fit)
+  if (S == 2 && mode != 0) return false;
   const size_t rb = f.rec_bytes;
   const int cpw = kLanes / S;
   const size_t tile = (size_t)f.num_features * 4 * cpw;
