@@ -29,6 +29,11 @@
  *     error has enqueued nothing.  Faults inside kernels surface at the
  *     caller's next synchronisation of the stream.
  *   - The device is the HIP device current on the calling thread.
+ *   - The scoring, selection and re-rank calls allocate nothing and only
+ *     enqueue kernels, so they may be captured into a HIP graph on the
+ *     stream, once each has run outside the capture on that device (its
+ *     first call sets kernel attributes).  Replays read and write the
+ *     buffers given at capture.
  *   - Errors are returned as status codes; ml2_last_error() gives a
  *     thread-local description of the last non-OK status.
  */
