@@ -3,7 +3,9 @@ replayed: every replay, with eager work and synchronizations between the
 replays, gives the eager step's outputs bit for bit, and a replay after the
 pool changed in place gives the eager outputs for the new pool.  Covers the
 one-pass kernel with the one-workgroup selection (Tiny) and the two walks
-with the multi-workgroup selection and its grid barrier (Medium)."""
+with the multi-workgroup selection and its grid barrier (Medium), each
+followed by a second-level re-rank of the selected rows (model A: here the
+V ensemble, over the same columns)."""
 import numpy as np
 import pytest
 
@@ -19,10 +21,17 @@ def _note(msg):
 
 
 class Step:
-    """ml2_score then ml2_filter_topk into buffers of its own."""
+    """ml2_score, ml2_filter_topk and ml2_rerank into buffers of its own."""
 
     def __init__(self, v, p, n, k, dev):
         self.v, self.p, self.k = v, p, k
+        self.keep = max(1, k // 2)
+        self.a_scores = torch.empty(k, dtype=torch.float32, device=dev)
+        self.a_idx = torch.empty(self.keep, dtype=torch.int32, device=dev)
+        self.a_top = torch.empty(self.keep, dtype=torch.float32, device=dev)
+        self.a_num = torch.empty(1, dtype=torch.int32, device=dev)
+        self.a_wsb = ml2.ml2_rerank_workspace_bytes(v, k)
+        self.a_ws = torch.empty(self.a_wsb, dtype=torch.uint8, device=dev)
         self.valid = torch.empty(n, dtype=torch.uint8, device=dev)
         self.score = torch.empty(n, dtype=torch.float32, device=dev)
         self.idx = torch.empty(k, dtype=torch.int32, device=dev)
@@ -35,6 +44,8 @@ class Step:
         ml2.ml2_score(self.v, self.p, X, self.valid, None, self.score)
         ml2.ml2_filter_topk(self.valid, self.score, self.k, self.idx, self.top, self.num,
                             self.ws, self.wsb, X.shape[0])
+        ml2.ml2_rerank(self.v, X, self.idx, self.keep, self.a_scores, self.a_idx, self.a_top,
+                       self.a_num, self.a_ws, self.a_wsb, m=self.k)
 
     def clear(self):
         self.valid.fill_(7)
@@ -42,11 +53,17 @@ class Step:
         self.idx.fill_(-5)
         self.top.fill_(float("nan"))
         self.num.fill_(-5)
+        for t in (self.a_scores, self.a_top):
+            t.fill_(float("nan"))
+        self.a_idx.fill_(-5)
+        self.a_num.fill_(-5)
 
     def outputs(self):
         return (self.valid.cpu().numpy(), self.score.cpu().numpy().view(np.uint32),
                 self.idx.cpu().numpy(), self.top.cpu().numpy().view(np.uint32),
-                self.num.cpu().numpy())
+                self.num.cpu().numpy(), self.a_scores.cpu().numpy().view(np.uint32),
+                self.a_idx.cpu().numpy(), self.a_top.cpu().numpy().view(np.uint32),
+                self.a_num.cpu().numpy())
 
 
 def _same(a, b):
