@@ -98,6 +98,27 @@ def copy_probe() -> None:
     print(json.dumps({"copy_probe_bytes": 4 * n, "launches": 5}))
 
 
+def copy_bandwidth(dev) -> float:
+    """A plain device-to-device copy of 1 GiB (torch's copy kernel), timed
+    with HIP events: bytes read + written per second (GB/s), median of 5."""
+    import torch
+    n = 1 << 28
+    a = torch.ones(n, dtype=torch.float32, device=dev)
+    b = torch.empty_like(a)
+    for _ in range(2):
+        b.copy_(a)
+    ts = []
+    for _ in range(5):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        b.copy_(a)
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    del a, b
+    return 2.0 * 4 * n / (float(np.median(ts)) / 1000.0) / 1e9
+
+
 def probes() -> None:
     """Microbenchmarks of the units the walks use (include/ml2_probe.h), as
     one JSON line: LDS bytes per clock per CU by read width and pattern,
@@ -347,7 +368,7 @@ def _print(out) -> int:
 
 
 def out_hbm(w, args, value, ms_per_step, t_val, t_perf, t_topk, n_valid, alg_bytes, fused,
-            traffic):
+            traffic, copy_gbs):
     """The HBM-bound diagnostic: small ensembles, so reading the pool bounds
     the step.  The roofline object covers the launch that reads every row
     once (4F bytes): with one pass the fused walk, which also writes the mask
@@ -377,8 +398,9 @@ def out_hbm(w, args, value, ms_per_step, t_val, t_perf, t_topk, n_valid, alg_byt
                 "work_per_launch": f"{f_bytes:.4g} bytes ({w.n} rows x {4 * w.F} B + mask + "
                                    "score)",
                 "launch_ms": t_val,
+                "copy_gbs": copy_gbs, "frac_of_copy": achieved / copy_gbs,
                 "step": {"algorithmic_bytes": alg_bytes, "achieved_gbs": step_gbs,
-                         "frac": step_gbs / HBM_PEAK_GBS},
+                         "frac": step_gbs / HBM_PEAK_GBS, "frac_of_copy": step_gbs / copy_gbs},
             },
             "hbm_frac": step_gbs / HBM_PEAK_GBS,
             "kernel_ms": {"validity_perf_one_pass": t_val, "topk": t_topk},
@@ -403,6 +425,7 @@ def out_hbm(w, args, value, ms_per_step, t_val, t_perf, t_topk, n_valid, alg_byt
             "frac": achieved / HBM_PEAK_GBS, "traffic": None,
             "work_per_launch": f"{val_bytes:.4g} bytes ({w.n} rows x {4 * w.F} B + mask)",
             "launch_ms": t_val,
+            "copy_gbs": copy_gbs, "frac_of_copy": achieved / copy_gbs,
             "perf_kernel": {"achieved": perf_bytes / (t_perf / 1000.0) / 1e9,
                             "launch_ms": t_perf,
                             "bytes": perf_bytes},
@@ -608,9 +631,10 @@ def main() -> int:
         t_perf = t_val
     perf_visits_per_s = visits_p / (t_perf / 1000.0)
     traffic = _traffic(sha, w.name)
+    copy_gbs = copy_bandwidth(dev)  # HBM fractions are also given against it
     if w.name == "hbm":
         res = out_hbm(w, args, value, ms_per_step, t_val, t_perf, t_topk, n_valid, alg_bytes,
-                      fused, traffic if fused else None)
+                      fused, traffic if fused else None, copy_gbs)
         res["config"].update(launch)
         return _print(res)
     shape = PERF_WALK_SHAPE.get(w.name)
@@ -649,7 +673,9 @@ def main() -> int:
         "hbm": {"algorithmic_bytes_per_step": alg_bytes,
                 "achieved_gbs": alg_bytes / (ms_per_step / 1000.0) / 1e9,
                 "peak_gbs": HBM_PEAK_GBS,
-                "frac": alg_bytes / (ms_per_step / 1000.0) / 1e9 / HBM_PEAK_GBS},
+                "frac": alg_bytes / (ms_per_step / 1000.0) / 1e9 / HBM_PEAK_GBS,
+                "copy_gbs": copy_gbs,
+                "frac_of_copy": alg_bytes / (ms_per_step / 1000.0) / 1e9 / copy_gbs},
     }
     out = {
         "metric": METRIC, "value": value, "unit": "candidates/s", "n_gpus": 1,
