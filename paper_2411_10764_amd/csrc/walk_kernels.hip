@@ -552,32 +552,42 @@ __device__ __forceinline__ float walk_slot_lanes(const char *slot, int ntr, int 
 __device__ __forceinline__ float walk_slot_single(const char *slot, const SlotHead &hd,
                                                   const char *tile_lane, float m) {
   const uint32_t *roots = reinterpret_cast<const uint32_t *>(slot + 16);
-  RWalks<1, 1> A;
-  A.u[0] = roots[0];
-  A.read_nodes(slot);
+  // a: byte offset of the lane's current node in the slot
+  uint32_t a = 8u * roots[0];
+  uint2 nd = *reinterpret_cast<const uint2 *>(slot + a);
   __builtin_amdgcn_sched_barrier(0);
+  const uint32_t end = 8u * hd.sentinel;
   const int cap = hd.ntrees * (hd.depth + 2) + 8;
   int it = 0;
   bool go = true;
   while (go) {
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
-      A.read_features(tile_lane);
+      const uint32_t w0 = nd.x;
+      // bits 15..0: the feature's byte offset in a 256-byte tile row (a
+      // leaf: the next root's byte offset, read and ignored)
+      const float x = *reinterpret_cast<const float *>(tile_lane + (w0 & 0xFFFFu));
       __builtin_amdgcn_sched_barrier(0);
-      const uint32_t w0 = A.nd[0].x;
+      // both next addresses before the feature value is in: the left child
+      // (the right one follows it), or a leaf's next root either way
       const bool leaf = RWalks<1, 1>::is_leaf(w0);
-      m = m + (leaf ? __uint_as_float(A.nd[0].y) : -0.0f);
-      const bool missing_left = (int32_t)w0 < 0 && __builtin_isnan(A.x[0]);
-      const bool right = !(A.x[0] < __uint_as_float(A.nd[0].y)) && !missing_left;
       const int32_t off = (int32_t)(w0 << 1) >> 17;  // bits 30..16, signed
-      uint32_t un = A.u[0] + (uint32_t)off + (right ? 1u : 0u);
-      asm volatile("" : "+v"(un));  // computed by every lane: no branch
-      A.u[0] = leaf ? (w0 & 0xFFFFu) >> 3 : un;  // a leaf: its next root
-      A.read_nodes(slot);
+      const uint32_t to_left = leaf ? (w0 & 0xFFFFu) : a + 8u * (uint32_t)off;
+      const uint32_t to_right = leaf ? (w0 & 0xFFFFu) : to_left + 8u;
+      m = m + (leaf ? __uint_as_float(nd.y) : -0.0f);
+      // right: x >= t where a missing x goes left (default-left, bit 31),
+      // not x < t otherwise (a missing x goes right); both candidates
+      // follow from the feature in one compare each
+      const float t = __uint_as_float(nd.y);
+      const uint32_t by_ge = (x >= t) ? to_right : to_left;
+      const uint32_t by_nlt = !(x < t) ? to_right : to_left;
+      a = (int32_t)w0 < 0 ? by_ge : by_nlt;
+      asm volatile("" : "+v"(a));  // computed by every lane: no branch
+      nd = *reinterpret_cast<const uint2 *>(slot + a);
       __builtin_amdgcn_sched_barrier(0);
     }
     it += 8;
-    go = !__all(A.u[0] == hd.sentinel) && it < cap;
+    go = !__all(a == end) && it < cap;
   }
   return m;
 }
