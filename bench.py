@@ -55,9 +55,11 @@ LDS_BYTES_PER_S = 256 * 256 * 2.4e9
 VISIT_PEAK_LDS = LDS_BYTES_PER_S / 12
 VISIT_PEAK_PER_S = min(VISIT_PEAK_VALU, VISIT_PEAK_LDS)
 MALL_BYTES = 256 << 20  # MI355X Infinity Cache: pools below it are flushed between steps
-# The perf walk's launch shape on the 16M pool (depth, trees per lane, lanes
-# per candidate, waves, features): the shape of the walk-loop probe.
-PERF_WALK_SHAPE = {"roofline": (8, 4, 2, 8, 128)}
+# The perf walk's launch shape (depth, trees per lane, lanes per candidate,
+# waves, features) where the walk-loop probe is built for it: the 16M pool,
+# the explorer workload (64 visible columns) and the Skewed pool (depth 10).
+PERF_WALK_SHAPE = {"roofline": (8, 4, 2, 8, 128), "explorer": (8, 8, 1, 8, 64),
+                   "skewed": (10, 4, 1, 6, 64)}
 METRIC = "candidate configs scored+filtered/sec (validity+perf+top-k); % of HBM peak"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "walk_traffic_16m.json")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2411_10764_amd", "csrc", "walk_kernels.hip")
@@ -230,7 +232,7 @@ def walk_loop_ceiling(shape):
     from paper_2411_10764_amd import ml2
     cus = torch.cuda.get_device_properties(0).multi_processor_count
     d, g, s_, waves, f = shape
-    ms, visits = ml2.ml2_probe_visit(d, g, s_, waves, f, 512 if d == 8 else 1024, 4 * cus)
+    ms, visits = ml2.ml2_probe_visit(d, g, s_, waves, f, {6: 1024, 8: 512, 10: 256}[d], 4 * cus)
     return visits / (ms * 1e-3) / 1e12
 
 

@@ -44,6 +44,10 @@ def test_probe_shape_is_the_perf_walk_shape():
     w = gen.WORKLOADS["roofline"]
     d, g, s, waves, f = bench.PERF_WALK_SHAPE["roofline"]
     assert d == w.p_depth and f == w.F and (g, s, waves) == (4, 2, 8)
+    # the other shapes: depth and the columns P reads of their workloads
+    for name, (d, g, s, waves, f) in bench.PERF_WALK_SHAPE.items():
+        w = gen.WORKLOADS[name]
+        assert d == w.p_depth and f == (w.K if w.visible_only else w.F)
 
 
 def test_mall_flush_applies_to_pools_below_the_cache():
