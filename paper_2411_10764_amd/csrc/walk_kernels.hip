@@ -251,6 +251,15 @@ __device__ __forceinline__ void wait_dma_and_barrier() {
   __syncthreads();
 }
 
+// A wave's own tile, written by its lanes and then read by them: the LDS
+// performs one wave's operations in issue order, so only the compiler must
+// keep the accesses on their side of this point (no instruction, no wait
+// for the other waves).
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+}
+
 // Lanes 0..31 receive the value of lanes 32..63 (v_permlane32_swap: the
 // second result holds the first operand's upper half in its lower half).
 __device__ __forceinline__ float from_upper_half(float v) {
@@ -1097,7 +1106,12 @@ validity_kernel(WalkArgs a) {
       } else if (active && h == 0) {
         load_row<S>(a, row, tile_lane);
       }
-      __syncthreads();
+      // a resident ensemble is staged once (stage_prime ends with a
+      // barrier) and a wave reads only its own tile
+      if constexpr (M == kResident || M == kResidentInline)
+        wave_sync();
+      else
+        __syncthreads();
       float m;
       if constexpr (M == kResident) {
         m = walk_chunk_after<D, G, S>(st.cur, a.ntrees, tile_lane, h, a.base,
@@ -1319,7 +1333,7 @@ fused_kernel(WalkArgs a) {
     const int64_t rn = ((tg + gridDim.x) * W + wave) * CPW + cl;
     pf.commit(a, row, h, tile_lane);
     pf.template load_batch<0>(a, rn, h);
-    __syncthreads();
+    wave_sync();  // the ensembles are staged; a wave reads only its own tile
     const float2 m = walk_split<D, G, S>(trees, a.ntrees, a.fold_trees, tile_lane, h, a.base,
                                          a.base2,
                                          [&](int g) { pf.load_after_group(a, rn, h, g); });
