@@ -1106,12 +1106,11 @@ validity_kernel(WalkArgs a) {
       } else if (active && h == 0) {
         load_row<S>(a, row, tile_lane);
       }
-      // a resident ensemble is staged once (stage_prime ends with a
-      // barrier) and a wave reads only its own tile
-      if constexpr (M == kResident || M == kResidentInline)
-        wave_sync();
-      else
-        __syncthreads();
+      // a wave reads only its own tile, and every round finds chunk 0
+      // complete in the buffer: staged once (stage_prime ends with a
+      // barrier), or restaged by the previous round's last advance, which
+      // ends with one
+      wave_sync();
       float m;
       if constexpr (M == kResident) {
         m = walk_chunk_after<D, G, S>(st.cur, a.ntrees, tile_lane, h, a.base,
