@@ -415,7 +415,7 @@ ml2_status ml2_score_perf(const ml2_ensemble *p_ens, const float *X, int64_t n, 
   if (n == 0) return ML2_OK;
   ml2::WalkPlan p;
   const char *why = nullptr;
-  if (!ml2::plan_walk(p_ens->f, n, cu_count(dev), &p, &why))
+  if (!ml2::plan_walk(p_ens->f, n, cu_count(dev), &p, &why, valid != nullptr))
     return fail(ML2_ERR_UNSUPPORTED, "ml2_score_perf: %s", why);
   hipError_t e = ml2::launch_perf(p_ens->f, p, X, n, ld, valid, score_out,
                                   static_cast<hipStream_t>(stream));
@@ -456,7 +456,7 @@ ml2_status ml2_score(const ml2_ensemble *v, const ml2_ensemble *p, const float *
   ml2::WalkPlan pv, pp;
   const char *why = nullptr;
   if (!ml2::plan_walk(v->f, n, cu_count(dev), &pv, &why) ||
-      !ml2::plan_walk(p->f, n, cu_count(dev), &pp, &why))
+      !ml2::plan_walk(p->f, n, cu_count(dev), &pp, &why, true))
     return fail(ML2_ERR_UNSUPPORTED, "ml2_score: %s", why);
   hipError_t e = ml2::launch_validity(v->f, pv, X, n, ld, valid_out, margin_out, s);
   if (e == hipSuccess) e = ml2::launch_perf(p->f, pp, X, n, ld, valid_out, score_out, s);
@@ -701,7 +701,7 @@ ml2_status ml2_explorer_round(ml2_explorer *ex, const float *X, int64_t ld, int3
     ml2::WalkPlan pv, pp;
     const char *why = nullptr;
     if (!ml2::plan_walk(ex->v->f, ex->n, cus, &pv, &why) ||
-        !ml2::plan_walk(ex->p->f, ex->n, cus, &pp, &why))
+        !ml2::plan_walk(ex->p->f, ex->n, cus, &pp, &why, true))
       return fail(ML2_ERR_UNSUPPORTED, "ml2_explorer_round: %s", why);
     e = ml2::launch_validity(ex->v->f, pv, X, ex->n, ld, ex->valid, nullptr, s);
     if (e == hipSuccess) e = ml2::launch_exclude(ex->valid, ex->n, ex->proposed, held, s);
@@ -883,7 +883,8 @@ ml2_status ml2_stream_explorer_chunk(ml2_stream_explorer *ex, const float *X, in
   const int cus = cu_count(dev);
   ml2::WalkPlan pv, pp;
   const char *why = nullptr;
-  if (!ml2::plan_walk(ex->v->f, m, cus, &pv, &why) || !ml2::plan_walk(ex->p->f, m, cus, &pp, &why))
+  if (!ml2::plan_walk(ex->v->f, m, cus, &pv, &why) ||
+      !ml2::plan_walk(ex->p->f, m, cus, &pp, &why, true))
     return fail(ML2_ERR_UNSUPPORTED, "ml2_stream_explorer_chunk: %s", why);
   const int h = ex->cur;
   hipError_t e = ml2::launch_validity(ex->v->f, pv, X, m, ld, ex->valid, nullptr, s);

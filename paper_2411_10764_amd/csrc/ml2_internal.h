@@ -45,7 +45,9 @@ struct WalkPlan {
 };
 
 // Returns false (and sets *why) if no plan fits the LDS of one workgroup.
-bool plan_walk(const Forest &f, int64_t n_work, int cu_count, WalkPlan *plan, const char **why);
+// survivors: the walk covers the rows a mask accepts out of n_work.
+bool plan_walk(const Forest &f, int64_t n_work, int cu_count, WalkPlan *plan, const char **why,
+               bool survivors = false);
 
 // Validity and performance in one pass over the pool (fused_kernel): false
 // where the two ensembles or the pool do not allow it.  nv, np: records of V
