@@ -1721,7 +1721,9 @@ hipError_t launch_fused_d(const WalkPlan &p, const WalkArgs &a, hipStream_t s) {
 // at most 128 features), and the W candidate tiles plus both ensembles'
 // trees (their sum rounded up to a whole number of groups) within one
 // workgroup's LDS.  Shapes tried: eight waves with one lane per candidate,
-// eight with two, then four of each; larger groups first.  *nv: V's trees,
+// eight with two, then four of each (a pool of less than one eight-wave
+// round per CU: four waves with two lanes first); larger groups first.  The
+// tuning overrides of the split and the waves apply here too.  *nv: V's trees,
 // *np: P's trees staged (all of them).
 bool plan_fused(const Forest &v, const Forest &p, int64_t n, int64_t ld, const float *X,
                 int cu_count, WalkPlan *plan, int *nv, int *np) {
@@ -1733,7 +1735,19 @@ bool plan_fused(const Forest &v, const Forest &p, int64_t n, int64_t ld, const f
   const size_t rb = v.rec_bytes;
   struct Shape { int s, w; };
   const Shape shapes[] = {{1, 8}, {2, 8}, {1, 4}, {2, 4}};
-  for (const Shape &sh : shapes) {
+  // A pool of less than one eight-wave round per CU leaves most CUs idle:
+  // four-wave workgroups with two lanes per candidate spread it over more
+  // CUs and halve each lane's chain of trees (Tiny: 0.025 -> 0.019 ms).
+  const Shape small[] = {{2, 4}, {2, 8}, {1, 8}, {1, 4}};
+  const bool few = n <= (int64_t)kLanes * 8 * cu_count;
+  // the tuning overrides force the split and the waves where they fit
+  const int want_s = get_tune(kTuneSplit), want_w = get_tune(kTuneWaves);
+  const Shape forced = {want_s ? want_s : 1, want_w};
+  const bool force = want_w > 0;
+  const Shape *list = force ? &forced : few ? small : shapes;
+  const int nshapes = force ? 1 : 4;
+  for (int si = 0; si < nshapes; ++si) {
+    const Shape &sh = list[si];
     for (int G : {8, 4, 2, 1}) {
       const int gs = G * sh.s;
       if (!group_allowed(D, G, sh.s) || kTreePad % gs != 0) continue;
