@@ -60,6 +60,9 @@ MALL_BYTES = 256 << 20  # MI355X Infinity Cache: pools below it are flushed betw
 # the explorer workload (64 visible columns) and the Skewed pool (depth 10).
 PERF_WALK_SHAPE = {"roofline": (8, 4, 2, 8, 128), "explorer": (8, 8, 1, 8, 64),
                    "skewed": (10, 4, 1, 6, 64)}
+# The validity walk's launch shape on the same pools.
+VALIDITY_WALK_SHAPE = {"roofline": (6, 8, 2, 8, 128), "explorer": (6, 8, 1, 8, 64),
+                       "skewed": (6, 8, 1, 8, 64)}
 METRIC = "candidate configs scored+filtered/sec (validity+perf+top-k); % of HBM peak"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "walk_traffic_16m.json")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2411_10764_amd", "csrc", "walk_kernels.hip")
@@ -641,6 +644,9 @@ def main() -> int:
         return _print(res)
     shape = PERF_WALK_SHAPE.get(w.name)
     loop = walk_loop_ceiling(shape) * 1e12 if shape else None
+    vshape = None if fused else VALIDITY_WALK_SHAPE.get(w.name)
+    vloop = walk_loop_ceiling(vshape) * 1e12 if vshape else None
+    v_visits_per_s = visits_v / (t_val / 1000.0)
     roofline = {
         "bound": "alu",
         "limiter": "lds",
@@ -670,8 +676,14 @@ def main() -> int:
                                       "features; ml2_probe_visit, timed live)"}
                              if loop else None),
         "validity_kernel": (None if fused else
-                            {"achieved": visits_v / (t_val / 1000.0) / 1e12, "launch_ms": t_val,
-                             "frac": visits_v / (t_val / 1000.0) / VISIT_PEAK_PER_S}),
+                            {"achieved": v_visits_per_s / 1e12, "launch_ms": t_val,
+                             "frac": v_visits_per_s / VISIT_PEAK_PER_S,
+                             "measured_ceiling": (
+                                 {"achieved": vloop / 1e12, "frac": v_visits_per_s / vloop,
+                                  "what": "walk loop alone at the validity walk's shape "
+                                          f"(depth {vshape[0]}, {vshape[1]} trees per lane, "
+                                          f"{vshape[2]} lanes per candidate, {vshape[3]} waves, "
+                                          f"{vshape[4]} features)"} if vloop else None)}),
         "hbm": {"algorithmic_bytes_per_step": alg_bytes,
                 "achieved_gbs": alg_bytes / (ms_per_step / 1000.0) / 1e9,
                 "peak_gbs": HBM_PEAK_GBS,

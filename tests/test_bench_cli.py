@@ -48,6 +48,11 @@ def test_probe_shape_is_the_perf_walk_shape():
     for name, (d, g, s, waves, f) in bench.PERF_WALK_SHAPE.items():
         w = gen.WORKLOADS[name]
         assert d == w.p_depth and f == (w.K if w.visible_only else w.F)
+    # the validity walk's: V's depth and the columns V reads
+    assert set(bench.VALIDITY_WALK_SHAPE) == set(bench.PERF_WALK_SHAPE)
+    for name, (d, g, s, waves, f) in bench.VALIDITY_WALK_SHAPE.items():
+        w = gen.WORKLOADS[name]
+        assert d == w.v_depth and f == (w.K if w.visible_only else w.F)
 
 
 def test_mall_flush_applies_to_pools_below_the_cache():
